@@ -1,0 +1,39 @@
+/*
+ * synth.h -- seeded synthetic replica gradients (the one input generator
+ * both the oracle and the HIP path consume).  Host-only C.
+ */
+#ifndef ASPIS_SYNTH_H
+#define ASPIS_SYNTH_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { SYNTH_ROLE_HONEST = 0, SYNTH_ROLE_REVERSED = 1, SYNTH_ROLE_ALIE = 2,
+       SYNTH_ROLE_NOISE = 3 };
+enum { SYNTH_DIST_NORMAL = 0, SYNTH_DIST_STUDENT3 = 1 };
+
+/* Philox4x32-10 block for a 64-bit seed (key) and a 128-bit counter. */
+void synth_philox(uint64_t seed, const uint32_t ctr[4], uint32_t out[4]);
+
+/* One 32-bit draw, for seeded choices (adversary sets, permutations). */
+uint32_t synth_u32(uint64_t seed, uint32_t stream, uint64_t index);
+
+/* Honest gradient g_file[k] and a noise value for (worker, file, k). */
+float synth_honest_value(uint64_t seed, int32_t dist, uint32_t file, uint64_t k);
+float synth_noise_value(uint64_t seed, uint32_t worker, uint32_t file, uint64_t k);
+
+/* Fill out[f][r][nk] with coordinates [k0, k0+nk) of every replica.
+ * role[i*r+s] picks the value of slot s of file i; worker[i*r+s] is the
+ * worker holding it (only the noise role uses it).  Returns 0 on success. */
+int synth_fill(const uint8_t *role, const int32_t *worker, int64_t f, int32_t r,
+               int64_t k0, int64_t nk, int32_t dist, uint64_t seed,
+               double alie_z, float *out, int32_t nthreads);
+
+uint64_t synth_fnv1a(const void *buf, int64_t nbytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
