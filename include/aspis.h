@@ -1,0 +1,205 @@
+/*
+ * aspis.h -- C ABI of libaspis: the parameter server's detect-and-aggregate
+ * step of Aspis (Konstantinidis & Ramamoorthy, "Aspis: Robust Detection for
+ * Distributed Learning", MLSys 2022) on one AMD Instinct MI355X (gfx950).
+ *
+ * Plain C: no C++ or torch types cross this boundary.  Device pointers are
+ * HIP device addresses (e.g. torch tensors' data_ptr()); "stream" is a
+ * hipStream_t passed as void* (NULL = the default stream).
+ *
+ * Symbols: K workers, r replicas per file (odd), q bound on adversaries,
+ * f = C(K,r) files, d gradient coordinates, P = r(r-1)/2 slot pairs.
+ *
+ * Layout of the replica tensor ("grads"): float32 [f][r][d], contiguous,
+ * row (i,s) = the gradient returned for file i by the worker in slot s,
+ * where slot s of file i is the s-th smallest worker of the file's subset.
+ *
+ * Ownership: every buffer is allocated and freed by the caller.  The library
+ * keeps no device memory between calls; what it needs beyond inputs and
+ * outputs comes through the caller's workspace.
+ *
+ * Errors: every entry point returns an aspis_status and never throws.  On
+ * ASPIS_ERR_INVALID_ARG / ASPIS_ERR_OVERFLOW nothing has been written or
+ * enqueued.  HIP failures return ASPIS_ERR_DEVICE.  aspis_last_error()
+ * returns a message for the calling thread's last failure.
+ *
+ * Asynchrony: aspis_detect and aspis_aggregate only enqueue work on the
+ * stream.  aspis_clique is host code.  aspis_detect_aggregate synchronises
+ * the stream twice (it needs the agreement graph on the host).
+ *
+ * Thread safety: re-entrant; the only global state is the per-thread error
+ * message.  Calls that share output buffers must not overlap.
+ */
+#ifndef ASPIS_H
+#define ASPIS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ASPIS_OK = 0,
+    ASPIS_ERR_INVALID_ARG = 1,   /* bad size, NULL pointer, unsupported r   */
+    ASPIS_ERR_OVERFLOW = 2,      /* f or f*r*d does not fit in int64         */
+    ASPIS_ERR_BUFFER_SMALL = 3,  /* caller buffer / workspace too small      */
+    ASPIS_ERR_DEVICE = 4,        /* a HIP call failed                        */
+    ASPIS_ERR_NO_FILES = 5       /* selection kept no file; out untouched    */
+} aspis_status;
+
+typedef enum {
+    ASPIS_REDUCE_MEDIAN = 0,     /* coordinate-wise (lower) median           */
+    ASPIS_REDUCE_MEAN = 1,       /* coordinate-wise mean                     */
+    ASPIS_REDUCE_PAPER = 2       /* mean on successful detection, else median */
+} aspis_reduce;
+
+/* Limits of this build. */
+#define ASPIS_MAX_K_DEVICE 64    /* K for the device entry points            */
+#define ASPIS_MAX_K_CLIQUE 128   /* K for aspis_clique                       */
+#define ASPIS_MAX_R 7            /* largest (odd) redundancy                 */
+
+/* Number of files f = C(K,r) (Section 3, Algorithm 2).
+ * Returns -1 if K < 1, r < 1, r > K, or the value exceeds int64. */
+int64_t aspis_num_files(int32_t K, int32_t r);
+
+/* Algorithm 2 (subset assignment), Example 1 fixing file 0 <-> {U1,U2,U3}:
+ * writes the f r-subsets of {0..K-1} in lexicographic order, members
+ * ascending: subsets[i*r + s] = worker of slot s of file i (host memory,
+ * caller-owned, at least cap_files*r entries).
+ * Errors: INVALID_ARG (K<1, r<1, r>K, NULL), OVERFLOW (f > int64),
+ * BUFFER_SMALL (f > cap_files; nothing written). */
+aspis_status aspis_assign(int32_t K, int32_t r, int32_t *subsets,
+                          int64_t cap_files);
+
+/* Detection outputs, all device pointers, caller-owned, written by
+ * aspis_detect / aspis_detect_aggregate.
+ *   pair_diff[f]    bit p set iff the replicas of slot pair p (pairs (s,t),
+ *                   s<t, in lexicographic order) differ in at least one
+ *                   coordinate -- the complement of the agreement indicator
+ *                   of Eq. (4), read bitwise.
+ *   vote[f]         Eq. (3): the slot carrying the majority value -- the
+ *                   lowest slot of the largest class of bitwise-equal
+ *                   replicas (ties between classes: the lower slot).
+ *   has_majority[f] 1 iff that class holds at least (r+1)/2 replicas.
+ *   disagree[K]     row bitsets of the K x K disagreement matrix: bit v of
+ *                   row u set iff workers u and v differ on at least one of
+ *                   their C(K-2,r-2) common files, i.e. no edge (u,v) in the
+ *                   detection graph of Section 4 (Eq. 5 below its maximum).
+ */
+typedef struct {
+    uint32_t *pair_diff;
+    int8_t *vote;
+    uint8_t *has_majority;
+    uint64_t *disagree;
+} aspis_detect_out;
+
+/* Section 4, Eq. (4)-(5) and Algorithm 3 (first loop), plus the per-file
+ * majority of Eq. (3): one pass over the replica tensor.
+ *   grads        device float32 [f][r][d] (see layout above)
+ *   subsets_dev  device int32 [f][r], the table of aspis_assign
+ *   out          device outputs above (all four required)
+ * Requires 2 <= K <= 64, r odd with 3 <= r <= min(K,7), d >= 1.
+ * Enqueues on stream; outputs are valid once the stream reaches them. */
+aspis_status aspis_detect(const float *grads, int32_t K, int32_t r, int64_t d,
+                          const int32_t *subsets_dev,
+                          const aspis_detect_out *out, void *stream);
+
+/* Outcome of Algorithm 3.  Bitsets hold worker u at word u/64, bit u%64. */
+typedef struct {
+    int32_t success;          /* exactly one maximum clique, of size >= K-q  */
+    int32_t omega;            /* size of a maximum clique                    */
+    int32_t n_maximum;        /* number of maximum cliques                   */
+    int32_t n_words;          /* (K+63)/64                                   */
+    int64_t n_maximal;        /* maximal cliques enumerated                  */
+    uint64_t honest[2];       /* H = the unique maximum clique (if success)  */
+    uint64_t detected[2];     /* A^ = U \ H (if success), else empty         */
+    uint64_t first[2];        /* the first maximum clique found              */
+} aspis_clique_result;
+
+/* Algorithm 3 (clique step), host only, synchronous: enumerates all maximal
+ * cliques of the detection graph (complement of the disagreement matrix) by
+ * Bron-Kerbosch with Tomita pivoting and decides success.
+ *   disagree_rows  host, K rows of n_words = (K+63)/64 uint64 each; the
+ *                  matrix must be symmetric with an empty diagonal
+ *   q              adversary bound, 0 <= q < K/2 (Section 2)
+ * Errors: INVALID_ARG (K outside [1,128], q outside [0,K/2), NULL,
+ * asymmetric matrix or set diagonal). */
+aspis_status aspis_clique(const uint64_t *disagree_rows, int32_t K, int32_t q,
+                          aspis_clique_result *res);
+
+/* Bytes of workspace aspis_aggregate and aspis_detect_aggregate need:
+ * f*(4+4+4) + 256, rounded up to 256. 0 on invalid arguments. */
+size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d);
+
+/* Algorithm 1, aggregation.  Selection: on success (Case 1) file i keeps
+ * the replica of its lowest slot whose worker is in H and is dropped when
+ * it has none; otherwise (Case 2) it keeps its majority vote.  Reduction:
+ * MEDIAN -> out[k] = element of rank floor((m-1)/2) of the m kept values
+ * under IEEE-754 totalOrder (-NaN < -inf < ... < -0 < +0 < ... < +NaN);
+ * MEAN -> out[k] = fl32(sum of the kept values in file order in fp64 / m);
+ * PAPER -> MEAN on success, MEDIAN otherwise.
+ *   det         detection outputs (vote is read on failure)
+ *   res         result of aspis_clique for the same round
+ *   out         device float32 [d]
+ *   sel_out     device int32 [f] (kept slot or -1) or NULL
+ *   n_selected  host, receives m (computed on the host, no sync) or NULL
+ *   workspace   device, >= aspis_aggregate_workspace() bytes, 256-aligned
+ * Errors: NO_FILES when m == 0 (out untouched), BUFFER_SMALL. */
+aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r,
+                             int64_t d, const int32_t *subsets_dev,
+                             const aspis_detect_out *det,
+                             const aspis_clique_result *res, aspis_reduce mode,
+                             float *out, int32_t *sel_out, int64_t *n_selected,
+                             void *workspace, size_t ws_bytes, void *stream);
+
+/* Timings (HIP events on the call's stream) and path taken by
+ * aspis_detect_aggregate. */
+typedef struct {
+    int32_t fused;             /* 1 if the single-pass kernel ran           */
+    int32_t speculation_hit;   /* 1 if the prefix guess was confirmed       */
+    int64_t probe_coords;      /* coordinates in the probe prefix           */
+    float ms_probe;            /* prefix agreement pass                     */
+    float ms_main;             /* main pass (fused, or detect + reduce)     */
+    float ms_fallback;         /* reduction rerun after a wrong guess       */
+    float ms_total;            /* first kernel to result, host steps incl.  */
+} aspis_run_stats;
+
+#define ASPIS_FLAG_TWO_PASS 1u   /* force detect, clique, then aggregate    */
+#define ASPIS_FLAG_TIMING 2u     /* fill the ms_* fields of stats           */
+
+/* The whole step in one call (Algorithm 3 then Algorithm 1): agreement,
+ * host clique, selection and reduction, with the same outputs as
+ * aspis_detect + aspis_clique + aspis_aggregate.  By default it reads the
+ * replica tensor once: it guesses the selection from a short coordinate
+ * prefix, reduces with that guess while checking agreement on all
+ * coordinates, and reruns the reduction if the full detection disagrees
+ * with the guess -- the result is exact either way.
+ *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
+ *   flags   ASPIS_FLAG_* ; stats may be NULL.
+ * Synchronises the stream (twice) before returning. */
+aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
+                                    int32_t q, int64_t d,
+                                    const int32_t *subsets_dev,
+                                    const aspis_detect_out *det,
+                                    aspis_reduce mode, float *out,
+                                    int32_t *sel_out, aspis_clique_result *res,
+                                    int64_t *n_selected, void *workspace,
+                                    size_t ws_bytes, uint32_t flags,
+                                    aspis_run_stats *stats, void *stream);
+
+/* Diagnostic: streams nbytes (multiple of 16) of device memory and writes a
+ * checksum word per thread to sink (device, >= aspis_read_probe_sink_words()
+ * uint32).  Used to measure the achievable HBM read bandwidth. */
+size_t aspis_read_probe_sink_words(void);
+aspis_status aspis_read_probe(const void *buf, size_t nbytes, uint32_t *sink,
+                              void *stream);
+
+/* Message describing the calling thread's last failure ("" if none). */
+const char *aspis_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ASPIS_H */

@@ -1,0 +1,433 @@
+// aspis_host.cpp -- C ABI of libaspis: argument checking, the host steps of
+// the method (Algorithm 2 assignment, Algorithm 3 clique enumeration) and the
+// orchestration of the gfx950 kernels (aspis_kernels.hip).
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "../../include/aspis.h"
+#include "aspis_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+aspis_status fail(aspis_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+aspis_status fail(aspis_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+#define ASPIS_HIP(call)                                                                  \
+    do {                                                                                 \
+        hipError_t e_ = (call);                                                          \
+        if (e_ != hipSuccess)                                                            \
+            return fail(ASPIS_ERR_DEVICE, "%s failed: %s", #call, hipGetErrorString(e_)); \
+    } while (0)
+
+// C(n,k) exactly, -1 when it exceeds int64.
+int64_t binom(int64_t n, int64_t k) {
+    if (k < 0 || n < 0 || k > n) return 0;
+    k = k < n - k ? k : n - k;
+    unsigned __int128 v = 1;
+    for (int64_t j = 0; j < k; ++j) {
+        v = v * (unsigned __int128)(n - j) / (unsigned __int128)(j + 1);
+        if (v > (unsigned __int128)INT64_MAX) return -1;
+    }
+    return (int64_t)v;
+}
+
+// Depth-first enumeration of r-subsets of {0..K-1}: emits them in
+// lexicographic order (smaller first member first, then recursively).
+void emit_subsets(int32_t K, int32_t r, int32_t depth, int32_t next, int32_t *cur,
+                  int32_t *&dst) {
+    if (depth == r) {
+        std::memcpy(dst, cur, sizeof(int32_t) * r);
+        dst += r;
+        return;
+    }
+    for (int32_t u = next; u <= K - (r - depth); ++u) {
+        cur[depth] = u;
+        emit_subsets(K, r, depth + 1, u + 1, cur, dst);
+    }
+}
+
+// ---- bitset clique enumeration (K <= 128) -------------------------------
+
+struct Bits {
+    uint64_t w[2];
+};
+inline Bits band(Bits a, Bits b) { return {{a.w[0] & b.w[0], a.w[1] & b.w[1]}}; }
+inline Bits bandnot(Bits a, Bits b) { return {{a.w[0] & ~b.w[0], a.w[1] & ~b.w[1]}}; }
+inline bool empty(Bits a) { return (a.w[0] | a.w[1]) == 0; }
+inline int popcount(Bits a) { return __builtin_popcountll(a.w[0]) + __builtin_popcountll(a.w[1]); }
+inline bool has(Bits a, int u) { return (a.w[u >> 6] >> (u & 63)) & 1u; }
+inline void set(Bits &a, int u) { a.w[u >> 6] |= 1ull << (u & 63); }
+inline void clr(Bits &a, int u) { a.w[u >> 6] &= ~(1ull << (u & 63)); }
+
+struct CliqueSearch {
+    int K;
+    Bits nbr[128];
+    int omega = 0;
+    int n_max = 0;
+    int64_t n_maximal = 0;
+    Bits first{{0, 0}};
+
+    void report(Bits R) {
+        ++n_maximal;
+        const int sz = popcount(R);
+        if (sz > omega) {
+            omega = sz;
+            n_max = 0;
+            first = R;
+        }
+        if (sz == omega) ++n_max;
+    }
+
+    // Bron-Kerbosch with Tomita pivoting: every maximal clique once.
+    void expand(Bits R, Bits P, Bits X) {
+        if (empty(P) && empty(X)) {
+            report(R);
+            return;
+        }
+        int pivot = -1, best = -1;
+        for (int half = 0; half < 2; ++half) {
+            uint64_t cand = P.w[half] | X.w[half];
+            while (cand) {
+                const int u = half * 64 + __builtin_ctzll(cand);
+                cand &= cand - 1;
+                const int c = popcount(band(P, nbr[u]));
+                if (c > best) {
+                    best = c;
+                    pivot = u;
+                }
+            }
+        }
+        Bits todo = bandnot(P, nbr[pivot]);
+        for (int half = 0; half < 2; ++half) {
+            uint64_t bits = todo.w[half];
+            while (bits) {
+                const int v = half * 64 + __builtin_ctzll(bits);
+                bits &= bits - 1;
+                Bits R2 = R;
+                set(R2, v);
+                expand(R2, band(P, nbr[v]), band(X, nbr[v]));
+                clr(P, v);
+                set(X, v);
+            }
+        }
+    }
+};
+
+aspis_status check_device_shape(int32_t K, int32_t r, int64_t d, int64_t *f_out) {
+    if (K < 2 || K > ASPIS_MAX_K_DEVICE)
+        return fail(ASPIS_ERR_INVALID_ARG, "K=%d outside [2,%d]", K, ASPIS_MAX_K_DEVICE);
+    if (r < 3 || r > ASPIS_MAX_R || r > K || (r % 2) == 0)
+        return fail(ASPIS_ERR_INVALID_ARG, "r=%d must be odd, 3 <= r <= min(K,%d)", r,
+                    ASPIS_MAX_R);
+    if (d < 1) return fail(ASPIS_ERR_INVALID_ARG, "d=%lld must be >= 1", (long long)d);
+    const int64_t f = binom(K, r);
+    if (f < 0) return fail(ASPIS_ERR_OVERFLOW, "C(%d,%d) overflows int64", K, r);
+    if (f * r > INT32_MAX)
+        return fail(ASPIS_ERR_OVERFLOW, "f*r=%lld exceeds int32 row indexing", (long long)(f * r));
+    if ((__int128)f * r * d > (__int128)INT64_MAX / 4)
+        return fail(ASPIS_ERR_OVERFLOW, "f*r*d overflows int64 bytes");
+    *f_out = f;
+    return ASPIS_OK;
+}
+
+uint64_t honest_mask(const aspis_clique_result *res) { return res->success ? res->honest[0] : 0ull; }
+
+// m = number of kept files, from the host-side clique outcome alone: on
+// success a file is dropped iff all its r workers are outside H, i.e. it is
+// one of the C(K-|H|, r) subsets of the detected set; otherwise every file
+// keeps its vote.
+int64_t kept_files(int32_t K, int32_t r, int64_t f, const aspis_clique_result *res) {
+    if (!res->success) return f;
+    const int h = __builtin_popcountll(res->honest[0]) + __builtin_popcountll(res->honest[1]);
+    return f - binom(K - h, r);
+}
+
+bool use_mean(aspis_reduce mode, const aspis_clique_result *res) {
+    return mode == ASPIS_REDUCE_MEAN || (mode == ASPIS_REDUCE_PAPER && res->success);
+}
+
+aspis_status check_detect_out(const aspis_detect_out *o) {
+    if (!o || !o->pair_diff || !o->vote || !o->has_majority || !o->disagree)
+        return fail(ASPIS_ERR_INVALID_ARG, "detect outputs must all be non-NULL");
+    return ASPIS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *aspis_last_error(void) { return g_err; }
+
+int64_t aspis_num_files(int32_t K, int32_t r) {
+    if (K < 1 || r < 1 || r > K) return -1;
+    return binom(K, r);
+}
+
+aspis_status aspis_assign(int32_t K, int32_t r, int32_t *subsets, int64_t cap_files) {
+    if (K < 1 || r < 1 || r > K || subsets == nullptr)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_assign: need 1 <= r <= K and a buffer");
+    const int64_t f = binom(K, r);
+    if (f < 0) return fail(ASPIS_ERR_OVERFLOW, "C(%d,%d) overflows int64", K, r);
+    if (f > cap_files)
+        return fail(ASPIS_ERR_BUFFER_SMALL, "need %lld files, buffer holds %lld", (long long)f,
+                    (long long)cap_files);
+    std::vector<int32_t> cur(r);
+    int32_t *dst = subsets;
+    emit_subsets(K, r, 0, 0, cur.data(), dst);
+    return ASPIS_OK;
+}
+
+aspis_status aspis_clique(const uint64_t *rows, int32_t K, int32_t q, aspis_clique_result *res) {
+    if (!rows || !res) return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: NULL argument");
+    if (K < 1 || K > ASPIS_MAX_K_CLIQUE)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: K=%d outside [1,%d]", K, ASPIS_MAX_K_CLIQUE);
+    if (q < 0 || 2 * q >= K)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: q=%d outside [0,K/2)", q);
+    const int nw = (K + 63) / 64;
+    auto bit = [&](int u, int v) { return (rows[u * nw + (v >> 6)] >> (v & 63)) & 1ull; };
+    for (int u = 0; u < K; ++u) {
+        if (bit(u, u)) return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: diagonal bit %d set", u);
+        for (int w = 0; w < nw; ++w) {
+            const int hi = K - 64 * w;
+            const uint64_t valid = hi >= 64 ? ~0ull : ((1ull << hi) - 1ull);
+            if (rows[u * nw + w] & ~valid)
+                return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: bits beyond K in row %d", u);
+        }
+        for (int v = u + 1; v < K; ++v)
+            if (bit(u, v) != bit(v, u))
+                return fail(ASPIS_ERR_INVALID_ARG, "aspis_clique: matrix not symmetric at (%d,%d)", u, v);
+    }
+    CliqueSearch cs;
+    cs.K = K;
+    Bits all{{0, 0}};
+    for (int u = 0; u < K; ++u) set(all, u);
+    for (int u = 0; u < K; ++u) {
+        Bits dis{{rows[u * nw], nw > 1 ? rows[u * nw + 1] : 0ull}};
+        Bits n = bandnot(all, dis);
+        clr(n, u);
+        cs.nbr[u] = n;
+    }
+    cs.expand(Bits{{0, 0}}, all, Bits{{0, 0}});
+    std::memset(res, 0, sizeof *res);
+    res->omega = cs.omega;
+    res->n_maximum = cs.n_max;
+    res->n_words = nw;
+    res->n_maximal = cs.n_maximal;
+    res->first[0] = cs.first.w[0];
+    res->first[1] = cs.first.w[1];
+    res->success = (cs.n_max == 1 && cs.omega >= K - q) ? 1 : 0;
+    if (res->success) {
+        res->honest[0] = cs.first.w[0];
+        res->honest[1] = cs.first.w[1];
+        Bits det = bandnot(all, cs.first);
+        res->detected[0] = det.w[0];
+        res->detected[1] = det.w[1];
+    }
+    g_err[0] = 0;
+    return ASPIS_OK;
+}
+
+size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d) {
+    int64_t f = 0;
+    if (check_device_shape(K, r, d, &f) != ASPIS_OK) return 0;
+    return aspis::workspace_bytes(f);
+}
+
+aspis_status aspis_detect(const float *grads, int32_t K, int32_t r, int64_t d,
+                          const int32_t *subsets_dev, const aspis_detect_out *out, void *stream) {
+    int64_t f = 0;
+    aspis_status st = check_device_shape(K, r, d, &f);
+    if (st != ASPIS_OK) return st;
+    if (!grads || !subsets_dev) return fail(ASPIS_ERR_INVALID_ARG, "aspis_detect: NULL input");
+    if ((st = check_detect_out(out)) != ASPIS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ASPIS_HIP(aspis::launch_fill_u32(out->pair_diff, f, 0u, s));
+    ASPIS_HIP(aspis::launch_fill_u64(out->disagree, K, 0ull, s));
+    ASPIS_HIP(aspis::launch_agree(grads, f, r, d, d, out->pair_diff, s));
+    ASPIS_HIP(aspis::launch_vote(out->pair_diff, subsets_dev, f, r, out->vote, out->has_majority,
+                                 out->disagree, s));
+    return ASPIS_OK;
+}
+
+aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d,
+                             const int32_t *subsets_dev, const aspis_detect_out *det,
+                             const aspis_clique_result *res, aspis_reduce mode, float *out,
+                             int32_t *sel_out, int64_t *n_selected, void *workspace,
+                             size_t ws_bytes, void *stream) {
+    int64_t f = 0;
+    aspis_status st = check_device_shape(K, r, d, &f);
+    if (st != ASPIS_OK) return st;
+    if (!grads || !subsets_dev || !det || !det->vote || !res || !out || !workspace)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_aggregate: NULL argument");
+    if (mode != ASPIS_REDUCE_MEDIAN && mode != ASPIS_REDUCE_MEAN && mode != ASPIS_REDUCE_PAPER)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_aggregate: unknown mode %d", (int)mode);
+    if (ws_bytes < aspis::workspace_bytes(f))
+        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f));
+    if (((uintptr_t)workspace & 255u) != 0)
+        return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (res->success && (res->honest[1] != 0 || K > 64))
+        return fail(ASPIS_ERR_INVALID_ARG, "honest set beyond worker 63");
+    const int64_t m = kept_files(K, r, f, res);
+    if (n_selected) *n_selected = m;
+    const bool mean = use_mean(mode, res);
+    if (!mean && aspis::pick_median_tile(f) == 0)
+        return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
+                    (long long)aspis::median_capacity(4));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    aspis::Workspace ws = aspis::carve_workspace(workspace, f);
+    ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success, honest_mask(res), ws,
+                                   false, sel_out, s));
+    if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
+    if (mean)
+        ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
+    else
+        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s));
+    return ASPIS_OK;
+}
+
+aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, int32_t q, int64_t d,
+                                    const int32_t *subsets_dev, const aspis_detect_out *det,
+                                    aspis_reduce mode, float *out, int32_t *sel_out,
+                                    aspis_clique_result *res, int64_t *n_selected, void *workspace,
+                                    size_t ws_bytes, uint32_t flags, aspis_run_stats *stats,
+                                    void *stream) {
+    using clk = std::chrono::steady_clock;
+    const auto t0 = clk::now();
+    int64_t f = 0;
+    aspis_status st = check_device_shape(K, r, d, &f);
+    if (st != ASPIS_OK) return st;
+    if (!grads || !subsets_dev || !out || !res || !workspace)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_detect_aggregate: NULL argument");
+    if ((st = check_detect_out(det)) != ASPIS_OK) return st;
+    if (q < 0 || 2 * q >= K) return fail(ASPIS_ERR_INVALID_ARG, "q=%d outside [0,K/2)", q);
+    if (mode != ASPIS_REDUCE_MEDIAN && mode != ASPIS_REDUCE_MEAN && mode != ASPIS_REDUCE_PAPER)
+        return fail(ASPIS_ERR_INVALID_ARG, "unknown mode %d", (int)mode);
+    if (ws_bytes < aspis::workspace_bytes(f))
+        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f));
+    if (((uintptr_t)workspace & 255u) != 0)
+        return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (mode != ASPIS_REDUCE_MEAN && aspis::pick_median_tile(f) == 0)
+        return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
+                    (long long)aspis::median_capacity(4));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool timing = stats && (flags & ASPIS_FLAG_TIMING);
+    aspis_run_stats local{};
+    hipEvent_t ev[6] = {};
+    if (timing)
+        for (auto &e : ev) ASPIS_HIP(hipEventCreate(&e));
+    auto destroy = [&]() {
+        if (timing)
+            for (auto &e : ev)
+                if (e) (void)hipEventDestroy(e);
+    };
+    std::vector<uint64_t> rows(K);
+    auto graph_to_host = [&](aspis_clique_result *out_res) -> aspis_status {
+        ASPIS_HIP(hipMemcpyAsync(rows.data(), det->disagree, sizeof(uint64_t) * K,
+                                 hipMemcpyDeviceToHost, s));
+        ASPIS_HIP(hipStreamSynchronize(s));
+        return aspis_clique(rows.data(), K, q, out_res);
+    };
+    aspis::Workspace ws = aspis::carve_workspace(workspace, f);
+
+    const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) && mode != ASPIS_REDUCE_MEAN &&
+                           aspis::fused_supported(f, r);
+    if (try_fused) {
+        // 1) agreement on a coordinate prefix -> provisional clique and selection
+        const int64_t probe = d < (int64_t(1) << 16) ? d : (int64_t(1) << 16);
+        local.probe_coords = probe;
+        if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
+        ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
+        ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
+        ASPIS_HIP(aspis::launch_agree(grads, f, r, d, probe, det->pair_diff, s));
+        ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote, det->has_majority,
+                                     det->disagree, s));
+        if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
+        aspis_clique_result guess{};
+        if ((st = graph_to_host(&guess)) != ASPIS_OK) { destroy(); return st; }
+        if (!use_mean(mode, &guess)) {
+            local.fused = 1;
+            ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, guess.success,
+                                           honest_mask(&guess), ws, false, nullptr, s));
+            // 2) one pass: agreement on every coordinate + median with the guess
+            ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
+            if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
+            ASPIS_HIP(aspis::launch_fused(grads, f, r, d, ws, det->pair_diff, out, s));
+            if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
+            ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
+            ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote,
+                                         det->has_majority, det->disagree, s));
+            if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
+            // 3) the final selection; the guess holds iff it selected the same
+            //    replica of every file and the reduction is still the median
+            const int64_t m = kept_files(K, r, f, res);
+            if (n_selected) *n_selected = m;
+            ASPIS_HIP(aspis::launch_fill_u32(reinterpret_cast<uint32_t *>(ws.flag), 1, 0u, s));
+            ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
+                                           honest_mask(res), ws, true, sel_out, s));
+            ASPIS_HIP(aspis::launch_compare_sel(ws.sel, ws.sel2, f, ws.flag, s));
+            int32_t flag = 0;
+            ASPIS_HIP(hipMemcpyAsync(&flag, ws.flag, sizeof flag, hipMemcpyDeviceToHost, s));
+            ASPIS_HIP(hipStreamSynchronize(s));
+            const bool hit = flag == 0 && !use_mean(mode, res);
+            local.speculation_hit = hit ? 1 : 0;
+            if (m == 0) { destroy(); return fail(ASPIS_ERR_NO_FILES, "selection kept no file"); }
+            if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
+            if (!hit) {
+                // ws.pos / ws.rows / ws.n_sel now describe the final selection
+                if (use_mean(mode, res))
+                    ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
+                else
+                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s));
+            }
+            if (timing) ASPIS_HIP(hipEventRecord(ev[5], s));
+            ASPIS_HIP(hipStreamSynchronize(s));
+            if (timing) {
+                ASPIS_HIP(hipEventElapsedTime(&local.ms_probe, ev[0], ev[1]));
+                ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));
+                ASPIS_HIP(hipEventElapsedTime(&local.ms_fallback, ev[4], ev[5]));
+            }
+            destroy();
+            local.ms_total = std::chrono::duration<float, std::milli>(clk::now() - t0).count();
+            if (stats) *stats = local;
+            return ASPIS_OK;
+        }
+    }
+    // two-pass: full agreement, clique, then selection and reduction
+    if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
+    if ((st = aspis_detect(grads, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) { destroy(); return st; }
+    if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
+    st = aspis_aggregate(grads, K, r, d, subsets_dev, det, res, mode, out, sel_out, n_selected,
+                         workspace, ws_bytes, stream);
+    if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
+    ASPIS_HIP(hipStreamSynchronize(s));
+    if (timing) ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));
+    destroy();
+    local.ms_total = std::chrono::duration<float, std::milli>(clk::now() - t0).count();
+    if (stats) *stats = local;
+    return st;
+}
+
+size_t aspis_read_probe_sink_words(void) { return aspis::read_probe_sink_words(); }
+
+aspis_status aspis_read_probe(const void *buf, size_t nbytes, uint32_t *sink, void *stream) {
+    if (!buf || !sink || nbytes % 16 != 0 || ((uintptr_t)buf & 15u))
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_read_probe: need 16-byte aligned buffer and size");
+    ASPIS_HIP(aspis::launch_read_probe(buf, nbytes, sink, static_cast<hipStream_t>(stream)));
+    return ASPIS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// aspis_internal.h -- launchers shared by the host library (aspis_host.cpp)
+// and the HIP kernels (aspis_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace aspis {
+
+// Median tile widths (coordinates per workgroup tile) this build supports.
+// The tile keeps every kept file's keys for T coordinates in LDS, so the
+// widest tile whose [files x T] key block fits is chosen.
+constexpr int kBlock = 256;                 // threads per workgroup
+constexpr int64_t kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
+
+// Largest number of kept files the LDS-tiled median supports for tile T.
+inline int64_t median_capacity(int T) { return kLdsBytes / (4 * (int64_t)T); }
+
+// Workspace layout (byte offsets) for f files.
+struct Workspace {
+    int32_t *sel;    // [f] kept slot or -1
+    int32_t *sel2;   // [f] second selection (to confirm a guessed one)
+    int32_t *pos;    // [f] row of the file in the kept-file list, or -1
+    int32_t *rows;   // [f] kept replica rows (i*r + slot), file order
+    int32_t *n_sel;  // [1] number of kept files
+    int32_t *flag;   // [1] scratch flag
+};
+size_t workspace_bytes(int64_t f);
+Workspace carve_workspace(void *base, int64_t f);
+
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
+
+// Pairwise agreement over coordinates [0, k_end) of every file; ORs the
+// per-file pair-difference bits into pair_diff (which the caller zeroes).
+hipError_t launch_agree(const float *g, int64_t f, int r, int64_t d,
+                        int64_t k_end, uint32_t *pair_diff, hipStream_t s);
+
+// Per-file vote / majority flag and the disagreement rows (caller zeroes
+// disagree).
+hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets,
+                       int64_t f, int r, int8_t *vote, uint8_t *has_majority,
+                       uint64_t *disagree, hipStream_t s);
+
+// Selection of Algorithm 1 into the workspace (sel, pos, rows, n_sel).
+// sel is written to ws.sel, or to ws.sel2 when into_sel2 is set, and also
+// to sel_out when it is not NULL.
+hipError_t launch_select(const int32_t *subsets, const int8_t *vote,
+                         int64_t f, int r, int success, uint64_t honest,
+                         const Workspace &ws, bool into_sel2, int32_t *sel_out,
+                         hipStream_t s);
+
+// Tile width the median kernel uses for up to f kept files (0: too many).
+int pick_median_tile(int64_t f);
+
+// Coordinate-wise lower median / fp64 mean of the kept rows.
+hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,
+                         int64_t f, float *out, hipStream_t s);
+hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
+                       float *out, hipStream_t s);
+
+// Single pass: agreement bits of every file over [0, d) and the median of
+// the rows selected by ws (a guess), in one read of the replica tensor.
+hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d,
+                        const Workspace &ws, uint32_t *pair_diff, float *out,
+                        hipStream_t s);
+bool fused_supported(int64_t f, int r);
+
+// Host-visible comparison of two selections (writes 1 to *flag if any
+// entry of a and b differ; the caller zeroes flag).
+hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
+                              int32_t *flag, hipStream_t s);
+
+size_t read_probe_sink_words();
+hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink,
+                             hipStream_t s);
+
+}  // namespace aspis

@@ -1,0 +1,649 @@
+// aspis_kernels.hip -- gfx950 kernels of the Aspis detect-and-aggregate step.
+//
+// The replica tensor is float32 [f][r][d]: row (i,s) holds the gradient the
+// worker in slot s returned for file i.  Everything here is integer work on
+// the 32-bit patterns (bitwise comparison, order-preserving keys) except the
+// fp64 sums of the mean, so nothing is a dense contraction and no MFMA is
+// used; the kernels are bound by HBM reads.
+//
+//   agree_kernel   Eq. (4): per file, OR over coordinates of "slot pair p
+//                  differs"; one coalesced stream over the r rows of a file.
+//   vote_kernel    Eq. (3) majority per file and the K x K disagreement rows
+//                  (Section 4: edge iff the pair agrees on all common files).
+//   select_kernel  Algorithm 1 selection (Case 1 honest replica / Case 2
+//                  majority) and the ordered list of kept rows.
+//   median_kernel  Algorithm 1 Case 2 coordinate-wise median: a tile of T
+//                  coordinates x all kept rows is staged in LDS as totalOrder
+//                  keys, then each column's lower median is found by an MSB
+//                  radix select run by G = 256/T lanes per column.
+//   fused_kernel   agree + median in one read: streams all r replicas of a
+//                  tile, compares them, and stages the guessed selection.
+//   mean_kernel    Algorithm 1 Case 1 mean, fp64 accumulation in file order.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "aspis_internal.h"
+
+namespace aspis {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// helpers
+
+// Order-preserving map of a binary32 bit pattern to an unsigned key:
+// unsigned order of keys == IEEE-754 totalOrder of the floats.
+__device__ __forceinline__ uint32_t to_key(uint32_t b) {
+    return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+__device__ __forceinline__ uint32_t from_key(uint32_t k) {
+    return (k & 0x80000000u) ? (k ^ 0x80000000u) : ~k;
+}
+
+template <int G>
+__device__ __forceinline__ uint32_t group_and(uint32_t v) {
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1) v &= (uint32_t)__shfl_xor((int)v, o, G);
+    return v;
+}
+template <int G>
+__device__ __forceinline__ uint32_t group_or(uint32_t v) {
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1) v |= (uint32_t)__shfl_xor((int)v, o, G);
+    return v;
+}
+template <int G>
+__device__ __forceinline__ int group_add(int v) {
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1) v += __shfl_xor(v, o, G);
+    return v;
+}
+
+// LDS layout of a [rows x T] key tile.  Row j lives at j*T; within the row,
+// column c is stored at c ^ swz(j) so that the G lanes working on one column
+// (rows j == g mod G) and the neighbouring columns of a half-wave hit
+// distinct banks.
+template <int T>
+__device__ __forceinline__ int tile_swz(int g) {
+    static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64, "tile width");
+    if constexpr (T == 4) {
+        return (g >> 3) & 3;                 // 64 lanes per column: 2-way at best
+    } else {
+        const int u = (T >= 32) ? g : g / (32 / T);
+        return u * (T / 8);                  // < T for every g < kBlock / T
+    }
+}
+
+// Lower median (rank floor((n-1)/2)) of each of the T columns of the LDS key
+// tile holding n rows; written to out[k0 + c] for k0 + c < d.
+// MSB-first radix select: the candidates of a column are split on the
+// highest bit where they still differ, the side holding the sought rank is
+// kept (compacted in place), until all candidates are equal.
+template <int T>
+__device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0,
+                                            int64_t d, float *out) {
+    constexpr int G = kBlock / T;
+    constexpr int STRIDE = G * T;     // words between a lane's rows (= kBlock)
+    const int tid = threadIdx.x;
+    const int g = tid % G;
+    const int c = tid / G;
+    const int col = c ^ tile_swz<T>(g);
+    uint32_t *base = tile + g * T + col;
+    int cnt = (n > g) ? (n - g + G - 1) / G : 0;
+    uint32_t m = (uint32_t)(n - 1) / 2;
+
+    uint32_t a = 0xFFFFFFFFu, o = 0u;
+    for (int x = 0; x < cnt; ++x) {
+        const uint32_t key = base[x * STRIDE];
+        a &= key;
+        o |= key;
+    }
+    a = group_and<G>(a);
+    o = group_or<G>(o);
+    uint32_t varying = a ^ o;
+    while (varying) {
+        const uint32_t bit = 1u << (31 - __clz(varying));
+        int z = 0;
+        for (int x = 0; x < cnt; ++x) z += (base[x * STRIDE] & bit) == 0u;
+        z = group_add<G>(z);
+        uint32_t want;
+        if (m < (uint32_t)z) {
+            want = 0u;
+        } else {
+            want = bit;
+            m -= (uint32_t)z;
+        }
+        int w = 0;
+        a = 0xFFFFFFFFu;
+        o = 0u;
+        for (int x = 0; x < cnt; ++x) {
+            const uint32_t key = base[x * STRIDE];
+            if ((key & bit) == want) {
+                base[w * STRIDE] = key;
+                ++w;
+                a &= key;
+                o |= key;
+            }
+        }
+        cnt = w;
+        a = group_and<G>(a);
+        o = group_or<G>(o);
+        varying = a ^ o;
+    }
+    if (g == 0 && k0 + c < d) out[k0 + c] = __uint_as_float(from_key(a));
+}
+
+// Load four consecutive coordinates [k, k+4) of one row as bit patterns;
+// coordinates at or beyond kend read as 0.
+template <bool VEC>
+__device__ __forceinline__ void load4(const float *row, int64_t k, int64_t kend,
+                                      uint32_t v[4]) {
+    if (VEC && k + 3 < kend) {
+        const float4 q = *reinterpret_cast<const float4 *>(row + k);
+        v[0] = __float_as_uint(q.x);
+        v[1] = __float_as_uint(q.y);
+        v[2] = __float_as_uint(q.z);
+        v[3] = __float_as_uint(q.w);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = (k + e < kend) ? __float_as_uint(row[k + e]) : 0u;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// utility kernels
+
+__global__ void fill_u32_kernel(uint32_t *p, int64_t n, uint32_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+__global__ void fill_u64_kernel(uint64_t *p, int64_t n, uint64_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// agreement: Eq. (4) for every file and slot pair, over coordinates [0,kend)
+
+constexpr int kAgreeUnroll = 4;                       // float4 per thread
+constexpr int64_t kAgreeChunk = (int64_t)kBlock * 4 * kAgreeUnroll;
+
+template <int R, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+agree_kernel(const float *__restrict__ g, int64_t f, int64_t d, int64_t kend,
+             int64_t nchunks, uint32_t *__restrict__ pair_diff) {
+    const int64_t nwork = f * nchunks;
+    for (int64_t w = blockIdx.x; w < nwork; w += gridDim.x) {
+        const int64_t i = w / nchunks;
+        const int64_t chunk = w - i * nchunks;
+        const float *rows = g + i * R * d;
+        uint32_t diff = 0u;
+#pragma unroll
+        for (int u = 0; u < kAgreeUnroll; ++u) {
+            const int64_t k = chunk * kAgreeChunk + (int64_t)u * kBlock * 4 +
+                              (int64_t)threadIdx.x * 4;
+            if (k < kend) {
+                uint32_t v[R][4];
+#pragma unroll
+                for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k, kend, v[s]);
+                int p = 0;
+#pragma unroll
+                for (int s = 0; s < R; ++s)
+#pragma unroll
+                    for (int t = s + 1; t < R; ++t) {
+                        const uint32_t x = (v[s][0] ^ v[t][0]) | (v[s][1] ^ v[t][1]) |
+                                           (v[s][2] ^ v[t][2]) | (v[s][3] ^ v[t][3]);
+                        diff |= (x != 0u ? 1u : 0u) << p;
+                        ++p;
+                    }
+            }
+        }
+        // OR over the wave; one atomic per wave only when something differs
+        uint32_t wdiff = 0u;
+        constexpr int P = R * (R - 1) / 2;
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            if (__ballot((diff >> p) & 1u)) wdiff |= 1u << p;
+        if ((threadIdx.x & 63) == 0 && wdiff) atomicOr(&pair_diff[i], wdiff);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// vote and disagreement rows
+
+__global__ void vote_kernel(const uint32_t *__restrict__ pair_diff,
+                            const int32_t *__restrict__ subsets, int64_t f,
+                            int r, int8_t *__restrict__ vote,
+                            uint8_t *__restrict__ has_majority,
+                            uint64_t *__restrict__ disagree) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < f;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const uint32_t pd = pair_diff[i];
+        // same[s] = bitmask of slots whose replica equals slot s's
+        uint32_t same[8];
+        for (int s = 0; s < r; ++s) same[s] = 1u << s;
+        int p = 0;
+        for (int s = 0; s < r; ++s)
+            for (int t = s + 1; t < r; ++t, ++p) {
+                if (pd >> p & 1u) {
+                    const int us = subsets[i * r + s], ut = subsets[i * r + t];
+                    atomicOr((unsigned long long *)&disagree[us], 1ull << ut);
+                    atomicOr((unsigned long long *)&disagree[ut], 1ull << us);
+                } else {
+                    same[s] |= 1u << t;
+                    same[t] |= 1u << s;
+                }
+            }
+        int best = 0, best_n = 0;
+        for (int s = 0; s < r; ++s) {
+            const int c = __popc(same[s]);
+            if (c > best_n) {
+                best_n = c;
+                best = s;
+            }
+        }
+        vote[i] = (int8_t)best;
+        has_majority[i] = (uint8_t)(best_n >= (r + 1) / 2);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// selection (one workgroup of 1024 threads; f is at most a few thousand)
+
+__global__ void __launch_bounds__(1024)
+select_kernel(const int32_t *__restrict__ subsets,
+              const int8_t *__restrict__ vote, int64_t f, int r,
+              int success, uint64_t honest, int32_t *__restrict__ sel,
+              int32_t *__restrict__ pos, int32_t *__restrict__ rows,
+              int32_t *__restrict__ n_sel, int32_t *__restrict__ sel_out) {
+    __shared__ int wave_tot[16];
+    __shared__ int carry;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) carry = 0;
+    __syncthreads();
+    for (int64_t b = 0; b < f; b += 1024) {
+        const int64_t i = b + tid;
+        int s = -1;
+        if (i < f) {
+            if (success) {
+                for (int x = 0; x < r; ++x)
+                    if (honest >> subsets[i * r + x] & 1ull) {
+                        s = x;
+                        break;
+                    }
+            } else {
+                s = vote[i];
+            }
+        }
+        const bool keep = s >= 0;
+        const uint64_t bal = __ballot(keep);
+        const int in_wave = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wave_tot[wave] = __popcll(bal);
+        __syncthreads();
+        int before = carry;
+        for (int w = 0; w < wave; ++w) before += wave_tot[w];
+        if (i < f) {
+            const int p = keep ? before + in_wave : -1;
+            sel[i] = s;
+            pos[i] = p;
+            if (sel_out) sel_out[i] = s;
+            if (keep) rows[p] = (int32_t)(i * r + s);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int tot = 0;
+            for (int w = 0; w < 16; ++w) tot += wave_tot[w];
+            carry += tot;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) *n_sel = carry;
+}
+
+__global__ void compare_sel_kernel(const int32_t *a, const int32_t *b, int64_t f,
+                                   int32_t *flag) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < f;
+         i += (int64_t)gridDim.x * blockDim.x)
+        if (a[i] != b[i]) *flag = 1;
+}
+
+// ---------------------------------------------------------------------------
+// median of the kept rows
+
+template <int T, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+median_kernel(const float *__restrict__ g, int64_t d,
+              const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
+              int64_t ntiles, float *__restrict__ out) {
+    extern __shared__ uint32_t tile[];
+    constexpr int G = kBlock / T;
+    constexpr int CPR = T / 4;           // float4 chunks per row segment
+    constexpr int RPI = kBlock / CPR;    // rows filled per sweep
+    const int n = *n_sel;
+    if (n <= 0) return;
+    const int tid = threadIdx.x;
+    const int cq = tid % CPR, j0 = tid / CPR;
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const int64_t k0 = t * T;
+        for (int j = j0; j < n; j += RPI) {
+            const float *row = g + (int64_t)rows[j] * d;
+            uint32_t v[4];
+            load4<VEC>(row, k0 + 4 * cq, d, v);
+            const int sw = tile_swz<T>(j % G);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(v[e]);
+        }
+        __syncthreads();
+        select_tile<T>(tile, n, k0, d, out);
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fused agreement + median (one read of all r replicas)
+
+template <int T, int R, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
+             const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
+             const int32_t *__restrict__ n_sel, int64_t ntiles,
+             uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
+    extern __shared__ uint32_t smem[];
+    constexpr int G = kBlock / T;
+    constexpr int CPR = T / 4;
+    constexpr int RPI = kBlock / CPR;
+    const int n = *n_sel;
+    uint32_t *tile = smem;
+    uint32_t *pd = smem + f * T;         // [f] per-workgroup pair-difference bits
+    const int tid = threadIdx.x;
+    for (int64_t i = tid; i < f; i += kBlock) pd[i] = 0u;
+    __syncthreads();
+    const int cq = tid % CPR, j0 = tid / CPR;
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const int64_t k0 = t * T;
+        for (int64_t i = j0; i < f; i += RPI) {
+            const float *rows = g + i * R * d;
+            uint32_t v[R][4];
+#pragma unroll
+            for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k0 + 4 * cq, d, v[s]);
+            uint32_t diff = 0u;
+            int p = 0;
+#pragma unroll
+            for (int s = 0; s < R; ++s)
+#pragma unroll
+                for (int u = s + 1; u < R; ++u) {
+                    const uint32_t x = (v[s][0] ^ v[u][0]) | (v[s][1] ^ v[u][1]) |
+                                       (v[s][2] ^ v[u][2]) | (v[s][3] ^ v[u][3]);
+                    diff |= (x != 0u ? 1u : 0u) << p;
+                    ++p;
+                }
+            if (diff) atomicOr(&pd[i], diff);
+            const int j = pos[i];
+            if (j >= 0) {
+                const int s_sel = sel[i];
+                uint32_t w[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    w[e] = v[0][e];
+#pragma unroll
+                    for (int s = 1; s < R; ++s) w[e] = (s_sel == s) ? v[s][e] : w[e];
+                }
+                const int sw = tile_swz<T>(j % G);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(w[e]);
+            }
+        }
+        __syncthreads();
+        if (n > 0) select_tile<T>(tile, n, k0, d, out);
+        __syncthreads();
+    }
+    for (int64_t i = tid; i < f; i += kBlock)
+        if (pd[i]) atomicOr(&pair_diff[i], pd[i]);
+}
+
+// ---------------------------------------------------------------------------
+// mean of the kept rows (fp64, file order)
+
+template <bool VEC>
+__global__ void __launch_bounds__(kBlock)
+mean_kernel(const float *__restrict__ g, int64_t d,
+            const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
+            float *__restrict__ out) {
+    const int n = *n_sel;
+    if (n <= 0) return;
+    const int64_t nquads = (d + 3) / 4;
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nquads;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = q * 4;
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int j = 0; j < n; ++j) {
+            uint32_t v[4];
+            load4<VEC>(g + (int64_t)rows[j] * d, k, d, v);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] += (double)__uint_as_float(v[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (k + e < d) out[k + e] = (float)(acc[e] / (double)n);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// read-bandwidth probe
+
+constexpr int kProbeBlocks = 2048;
+
+__global__ void __launch_bounds__(kBlock)
+read_probe_kernel(const uint4 *__restrict__ p, int64_t n16, uint32_t *sink) {
+    uint32_t acc = 0u;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const uint4 v = p[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    sink[blockIdx.x * (int64_t)blockDim.x + threadIdx.x] = acc;
+}
+
+int g_num_cus = 0;
+
+int num_cus() {
+    if (g_num_cus == 0) {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) ==
+                hipSuccess &&
+            cus > 0)
+            g_num_cus = cus;
+        else
+            g_num_cus = 256;
+    }
+    return g_num_cus;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int64_t grid_for(int64_t work, int64_t cap) { return work < cap ? (work < 1 ? 1 : work) : cap; }
+
+// widest tile T whose [rows x T] key block (plus extra bytes) fits in LDS
+int pick_tile(int64_t rows, int64_t extra_bytes) {
+    for (int T : {64, 32, 16, 8, 4})
+        if (rows * 4 * (int64_t)T + extra_bytes <= kLdsBytes) return T;
+    return 0;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// launchers
+
+size_t workspace_bytes(int64_t f) {
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    return up((size_t)f * 4) * 4 + 256;
+}
+
+int pick_median_tile(int64_t f) { return pick_tile(f, 0); }
+
+Workspace carve_workspace(void *base, int64_t f) {
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    char *p = static_cast<char *>(base);
+    Workspace w;
+    w.sel = reinterpret_cast<int32_t *>(p);
+    p += up((size_t)f * 4);
+    w.sel2 = reinterpret_cast<int32_t *>(p);
+    p += up((size_t)f * 4);
+    w.pos = reinterpret_cast<int32_t *>(p);
+    p += up((size_t)f * 4);
+    w.rows = reinterpret_cast<int32_t *>(p);
+    p += up((size_t)f * 4);
+    w.n_sel = reinterpret_cast<int32_t *>(p);
+    w.flag = w.n_sel + 1;
+    return w;
+}
+
+hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    fill_u32_kernel<<<(unsigned)grid_for((n + 255) / 256, 1024), 256, 0, s>>>(p, n, v);
+    return hipGetLastError();
+}
+hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    fill_u64_kernel<<<(unsigned)grid_for((n + 255) / 256, 1024), 256, 0, s>>>(p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_agree(const float *g, int64_t f, int r, int64_t d, int64_t kend,
+                        uint32_t *pair_diff, hipStream_t s) {
+    if (kend <= 0 || f <= 0) return hipSuccess;
+    const int64_t nchunks = (kend + kAgreeChunk - 1) / kAgreeChunk;
+    const unsigned grid = (unsigned)grid_for(f * nchunks, (int64_t)num_cus() * 16);
+    const bool vec = (d % 4 == 0) && aligned16(g);
+#define ASPIS_AGREE(RR)                                                              \
+    if (vec)                                                                         \
+        agree_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, f, d, kend, nchunks, pair_diff); \
+    else                                                                             \
+        agree_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, f, d, kend, nchunks, pair_diff);
+    switch (r) {
+    case 3: ASPIS_AGREE(3) break;
+    case 5: ASPIS_AGREE(5) break;
+    case 7: ASPIS_AGREE(7) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_AGREE
+    return hipGetLastError();
+}
+
+hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets, int64_t f,
+                       int r, int8_t *vote, uint8_t *has_majority, uint64_t *disagree,
+                       hipStream_t s) {
+    vote_kernel<<<(unsigned)grid_for((f + 255) / 256, 64), 256, 0, s>>>(
+        pair_diff, subsets, f, r, vote, has_majority, disagree);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const int32_t *subsets, const int8_t *vote, int64_t f, int r,
+                         int success, uint64_t honest, const Workspace &ws, bool into_sel2,
+                         int32_t *sel_out, hipStream_t s) {
+    select_kernel<<<1, 1024, 0, s>>>(subsets, vote, f, r, success, honest,
+                                     into_sel2 ? ws.sel2 : ws.sel, ws.pos, ws.rows, ws.n_sel,
+                                     sel_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
+                              int32_t *flag, hipStream_t s) {
+    compare_sel_kernel<<<(unsigned)grid_for((f + 255) / 256, 64), 256, 0, s>>>(a, b, f, flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
+                         float *out, hipStream_t s) {
+    const int T = pick_tile(f, 0);
+    if (T == 0) return hipErrorInvalidValue;
+    const int64_t ntiles = (d + T - 1) / T;
+    const size_t lds = (size_t)f * 4 * T;
+    const int per_cu = (int)(kLdsBytes / (int64_t)(lds ? lds : 1));
+    const unsigned grid =
+        (unsigned)grid_for(ntiles, (int64_t)num_cus() * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
+    const bool vec = (d % 4 == 0) && aligned16(g);
+#define ASPIS_MED(TT)                                                                      \
+    if (vec)                                                                               \
+        median_kernel<TT, true><<<grid, kBlock, lds, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out); \
+    else                                                                                   \
+        median_kernel<TT, false><<<grid, kBlock, lds, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+    switch (T) {
+    case 64: ASPIS_MED(64) break;
+    case 32: ASPIS_MED(32) break;
+    case 16: ASPIS_MED(16) break;
+    case 8: ASPIS_MED(8) break;
+    case 4: ASPIS_MED(4) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_MED
+    return hipGetLastError();
+}
+
+bool fused_supported(int64_t f, int r) {
+    return (r == 3 || r == 5 || r == 7) && pick_tile(f, f * 4) != 0;
+}
+
+hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Workspace &ws,
+                        uint32_t *pair_diff, float *out, hipStream_t s) {
+    const int T = pick_tile(f, f * 4);
+    if (T == 0) return hipErrorInvalidValue;
+    const int64_t ntiles = (d + T - 1) / T;
+    const size_t lds = (size_t)f * 4 * T + (size_t)f * 4;
+    const int per_cu = (int)(kLdsBytes / (int64_t)lds);
+    const unsigned grid =
+        (unsigned)grid_for(ntiles, (int64_t)num_cus() * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
+    const bool vec = (d % 4 == 0) && aligned16(g);
+#define ASPIS_FUSED(TT, RR)                                                                  \
+    if (vec)                                                                                 \
+        fused_kernel<TT, RR, true><<<grid, kBlock, lds, s>>>(g, f, d, ws.sel, ws.pos, ws.n_sel, \
+                                                             ntiles, pair_diff, out);        \
+    else                                                                                     \
+        fused_kernel<TT, RR, false><<<grid, kBlock, lds, s>>>(g, f, d, ws.sel, ws.pos,        \
+                                                              ws.n_sel, ntiles, pair_diff, out);
+#define ASPIS_FUSED_R(TT)                     \
+    switch (r) {                              \
+    case 3: ASPIS_FUSED(TT, 3) break;         \
+    case 5: ASPIS_FUSED(TT, 5) break;         \
+    case 7: ASPIS_FUSED(TT, 7) break;         \
+    default: return hipErrorInvalidValue;     \
+    }
+    switch (T) {
+    case 64: ASPIS_FUSED_R(64) break;
+    case 32: ASPIS_FUSED_R(32) break;
+    case 16: ASPIS_FUSED_R(16) break;
+    case 8: ASPIS_FUSED_R(8) break;
+    case 4: ASPIS_FUSED_R(4) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_FUSED_R
+#undef ASPIS_FUSED
+    return hipGetLastError();
+}
+
+hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws, float *out,
+                       hipStream_t s) {
+    const int64_t nquads = (d + 3) / 4;
+    const unsigned grid = (unsigned)grid_for((nquads + kBlock - 1) / kBlock, (int64_t)num_cus() * 8);
+    if ((d % 4 == 0) && aligned16(g))
+        mean_kernel<true><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out);
+    else
+        mean_kernel<false><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out);
+    return hipGetLastError();
+}
+
+size_t read_probe_sink_words() { return (size_t)kProbeBlocks * kBlock; }
+
+hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink, hipStream_t s) {
+    read_probe_kernel<<<kProbeBlocks, kBlock, 0, s>>>(static_cast<const uint4 *>(buf),
+                                                      (int64_t)(nbytes / 16), sink);
+    return hipGetLastError();
+}
+
+}  // namespace aspis

@@ -4,7 +4,8 @@ This is the single input generator that both the oracle and the HIP path
 consume.  It holds none of the method's arithmetic: the file->worker table is
 passed in by the caller, and this module only decides which replica carries
 which value (the attack simulation of Section 4.1 / 4.2 of the paper) and
-writes the numbers (``synth.c``).
+writes the numbers (``synth.hip``: a host fill for the oracle and a GPU fill
+that writes the same bytes straight into device memory).
 
 Workloads (shapes of the paper's CIFAR-10 / ResNet-18 experiments, r = 3):
 
@@ -54,6 +55,10 @@ def _load():
     lib.synth_honest_value.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint32,
                                        ctypes.c_uint64]
     lib.synth_honest_value.restype = ctypes.c_float
+    lib.synth_fill_device.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
+                                      ctypes.c_int32, ctypes.c_uint64, ctypes.c_double,
+                                      ctypes.c_int32, P, P, P]
+    lib.synth_fill_device.restype = ctypes.c_int
     lib.synth_fnv1a.argtypes = [P, ctypes.c_int64]
     lib.synth_fnv1a.restype = ctypes.c_uint64
     _lib = lib
@@ -210,6 +215,33 @@ def fill(role: np.ndarray, worker: np.ndarray, k0: int, nk: int, dist: int,
                             seed, alie_z, out.ctypes.data, nthreads)
     if rc != 0:
         raise RuntimeError(f"synth_fill failed ({rc})")
+    return out
+
+
+def fill_device(role: np.ndarray, worker: np.ndarray, out, dist: int, seed: int = SEED,
+                alie_z: float = 1.0):
+    """Write every replica of all d coordinates into the device tensor
+    ``out`` (contiguous float32 [f, r, d]) -- the same bytes as ``fill``."""
+    import torch
+    role = np.ascontiguousarray(role, dtype=np.uint8)
+    worker = np.ascontiguousarray(worker, dtype=np.int32)
+    f, r = role.shape
+    if not (out.is_cuda and out.dtype == torch.float32 and out.is_contiguous()
+            and out.dim() == 3 and tuple(out.shape[:2]) == (f, r)):
+        raise ValueError("out must be a contiguous cuda float32 [f, r, d] tensor")
+    d = out.shape[2]
+    dev = out.device
+    role_d = torch.from_numpy(role).to(dev)
+    worker_d = torch.from_numpy(worker).to(dev)
+    need_alie = int((role == ROLE_ALIE).any())
+    alie = torch.empty(d if need_alie else 1, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    rc = _load().synth_fill_device(role_d.data_ptr(), worker_d.data_ptr(), f, r, d, dist, seed,
+                                   alie_z, need_alie, alie.data_ptr(), out.data_ptr(), stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_device failed ({rc})")
+    torch.cuda.current_stream().synchronize()
+    del alie, role_d, worker_d
     return out
 
 

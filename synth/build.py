@@ -1,25 +1,31 @@
-"""Build the synthetic-input generator (plain C, gcc, pthreads)."""
+"""Build the synthetic-input generator (host fill + bit-identical GPU fill)."""
 import os
 import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libsynth.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 
 def build(verbose: bool = False) -> str:
-    src = os.path.join(HERE, "synth.c")
+    src = os.path.join(HERE, "synth.hip")
     tmp = LIB + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
-           "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
-           "-o", tmp, src, "-lm"]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O2", "-std=c++17", "-fPIC", "-shared", "-pthread",
+           "-ffp-contract=off", "-fno-fast-math", "-Wall",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-o", tmp, src]
     if verbose:
         print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    msgs = [ln for ln in (r.stdout + r.stderr).splitlines()
+            if ln.strip() and "packed-fp32-ops" not in ln]
+    if r.returncode != 0:
+        sys.stderr.write("\n".join(msgs) + "\n")
+        raise RuntimeError("hipcc failed building libsynth.so")
     os.replace(tmp, LIB)
     return LIB
 
 
 if __name__ == "__main__":
     build(verbose=True)
-    sys.exit(0)

@@ -1,6 +1,7 @@
 /*
  * synth.h -- seeded synthetic replica gradients (the one input generator
- * both the oracle and the HIP path consume).  Host-only C.
+ * both the oracle and the HIP path consume).  Host fill and a bit-identical
+ * device fill.
  */
 #ifndef ASPIS_SYNTH_H
 #define ASPIS_SYNTH_H
@@ -13,9 +14,6 @@ extern "C" {
 enum { SYNTH_ROLE_HONEST = 0, SYNTH_ROLE_REVERSED = 1, SYNTH_ROLE_ALIE = 2,
        SYNTH_ROLE_NOISE = 3 };
 enum { SYNTH_DIST_NORMAL = 0, SYNTH_DIST_STUDENT3 = 1 };
-
-/* Philox4x32-10 block for a 64-bit seed (key) and a 128-bit counter. */
-void synth_philox(uint64_t seed, const uint32_t ctr[4], uint32_t out[4]);
 
 /* One 32-bit draw, for seeded choices (adversary sets, permutations). */
 uint32_t synth_u32(uint64_t seed, uint32_t stream, uint64_t index);
@@ -30,6 +28,13 @@ float synth_noise_value(uint64_t seed, uint32_t worker, uint32_t file, uint64_t 
 int synth_fill(const uint8_t *role, const int32_t *worker, int64_t f, int32_t r,
                int64_t k0, int64_t nk, int32_t dist, uint64_t seed,
                double alie_z, float *out, int32_t nthreads);
+
+/* Same bytes as synth_fill for all d coordinates, written on the GPU into
+ * out_dev[f][r][d].  role_dev / worker_dev are device copies of the tables;
+ * alie_dev is device scratch of d floats (needed when need_alie). */
+int synth_fill_device(const uint8_t *role_dev, const int32_t *worker_dev, int64_t f,
+                      int32_t r, int64_t d, int32_t dist, uint64_t seed, double alie_z,
+                      int32_t need_alie, float *alie_dev, float *out_dev, void *stream);
 
 uint64_t synth_fnv1a(const void *buf, int64_t nbytes);
 

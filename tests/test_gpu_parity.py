@@ -1,0 +1,198 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, element by
+element, on seeded inputs that span several tiles and a ragged tail, plus
+special values, planted bit flips, every tile width and the fallback of the
+single-pass kernel."""
+from math import comb
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2108_02416_amd import aspis
+
+from _helpers import assert_detection, assert_same_floats, device, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(g: np.ndarray, K: int, r: int, q: int, mode: str, path: str):
+    import torch
+    gd = torch.from_numpy(np.ascontiguousarray(g)).to(device())
+    if path == "entry_points":
+        bufs = aspis.detect(gd, K, r)
+        torch.cuda.synchronize()
+        res = aspis.clique(to_np(bufs.disagree).view(np.uint64), K, q)
+        sel = torch.empty(g.shape[0], dtype=torch.int32, device=gd.device)
+        out, n = aspis.aggregate(gd, K, r, bufs, res, mode, sel_out=sel)
+        torch.cuda.synchronize()
+        return {"bufs": bufs, "clique": res, "out": out, "sel": sel, "n_selected": n,
+                "stats": {}}
+    flags = aspis.FLAG_TWO_PASS if path == "two_pass" else 0
+    got = aspis.detect_aggregate(gd, K, r, q, mode=mode, flags=flags | aspis.FLAG_TIMING)
+    torch.cuda.synchronize()
+    return got
+
+
+def _check(g, K, r, q, mode, path, nan_equal=False):
+    ref = oracle.run(g, K, r, q, mode=mode)
+    got = _run(g, K, r, q, mode, path)
+    assert_detection(got, ref, K)
+    assert (to_np(got["sel"]) == ref["sel"]).all()
+    assert got["n_selected"] == ref["n_selected"]
+    assert_same_floats(to_np(got["out"]), ref["out"], nan_equal=nan_equal)
+    return got, ref
+
+
+_D = {1: 4099, 2: 2053, 3: 1543, 4: 523, 5: 389}
+
+
+@pytest.mark.parametrize("path", ["fused", "two_pass", "entry_points"])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_workloads_small(idx, path):
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D[idx])
+    print(f"workload {idx} d={_D[idx]} path={path}", flush=True)
+    _check(g, wl.K, wl.r, wl.q, "median", path)
+
+
+@pytest.mark.parametrize("mode", ["mean", "paper"])
+@pytest.mark.parametrize("idx", [1, 3, 4])
+def test_workloads_small_modes(idx, mode):
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D[idx])
+    _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    _check(g, wl.K, wl.r, wl.q, mode, "two_pass")
+
+
+_SPECIAL = np.array([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 3.4e38, -3.4e38],
+                    dtype=np.float32)
+_NANS = np.array([0x7FC00000, 0x7FC00001, 0xFFC00000, 0x7F800001, 0xFFFFFFFF],
+                 dtype=np.uint32).view(np.float32)
+
+
+def _random_case(seed: int):
+    rng = np.random.default_rng(1000 + seed)
+    r = int(rng.choice([3, 3, 5, 7]))
+    K = int(rng.integers(max(r, 3), 13 if r < 7 else 10))
+    q = int(rng.integers(0, (K + 1) // 2))
+    d = int(rng.choice([1, 2, 3, 5, 17, 63, 64, 65, 255, 257, 1000, 4097]))
+    f = comb(K, r)
+    # per file, a random partition of the slots into classes of equal replicas
+    g = np.empty((f, r, d), dtype=np.float32)
+    for i in range(f):
+        labels = rng.integers(0, rng.integers(1, r + 1), size=r)
+        base = (rng.standard_normal((r, d)) * 0.01).astype(np.float32)
+        pick = rng.random((r, d))
+        base[pick < 0.05] = rng.choice(_SPECIAL, size=int((pick < 0.05).sum()))
+        if seed % 3 == 0:
+            base[pick > 0.98] = rng.choice(_NANS, size=int((pick > 0.98).sum()))
+        for s in range(r):
+            g[i, s] = base[labels[s]]
+    if seed % 4 == 1:           # single-bit flips at the first / last coordinate
+        for _ in range(3):
+            i, s = int(rng.integers(f)), int(rng.integers(r))
+            g.view(np.uint32)[i, s, int(rng.choice([0, d - 1]))] ^= np.uint32(1 << int(rng.integers(32)))
+    if seed % 5 == 2:           # a few workers send noise on every file (weak attack)
+        bad = rng.choice(K, size=q, replace=False)
+        subsets = oracle.assign(K, r)
+        for i in range(f):
+            for s in range(r):
+                if subsets[i, s] in bad:
+                    g[i, s] = rng.standard_normal(d).astype(np.float32)
+    return g, K, r, q
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_properties(seed):
+    g, K, r, q = _random_case(seed)
+    print(f"seed={seed} K={K} r={r} q={q} d={g.shape[2]}", flush=True)
+    for path in ("fused", "two_pass"):
+        _check(g, K, r, q, "median", path)
+    _check(g, K, r, q, "mean", "two_pass", nan_equal=True)
+
+
+@pytest.mark.parametrize("K,r,d", [(26, 3, 301), (32, 3, 97), (9, 7, 333), (13, 5, 129)])
+def test_tile_widths(K, r, d):
+    """f = 2600 (8-wide tiles), 4960 (4-wide), r = 5 and 7."""
+    q = (K - 1) // 2 - 1
+    rng = np.random.default_rng(K * 100 + r)
+    f = comb(K, r)
+    g = np.repeat((rng.standard_normal((f, 1, d)) * 0.01).astype(np.float32), r, axis=1)
+    s = oracle.assign(K, r)
+    bad = set(range(q))
+    for i in range(f):
+        for x in range(r):
+            if s[i, x] in bad:
+                g[i, x] *= np.float32(-100.0)
+    for path in ("fused", "two_pass"):
+        _check(g, K, r, q, "median", path)
+
+
+def test_guess_from_prefix_is_wrong_then_corrected():
+    """The single-pass path guesses the selection from the first 65,536
+    coordinates; a worker that deviates only after them makes the guess wrong
+    and the reduction must be redone with the final selection."""
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = 65536 + 777
+    g, info = synth.generate(wl, s, d=d)
+    # honest worker 5 flips one bit of every file it holds, late in the vector
+    for i in range(s.shape[0]):
+        for x in range(wl.r):
+            if s[i, x] == 5:
+                g.view(np.uint32)[i, x, d - 3] ^= np.uint32(0x10)
+    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused")
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+    assert not ref["clique"]["success"] or ref["clique"]["cliques"][0] != frozenset(range(2, 7))
+
+
+def test_guess_holds_on_clean_prefix():
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=65536 + 999)
+    got, _ = _check(g, wl.K, wl.r, wl.q, "median", "fused")
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 1
+
+
+def test_deterministic_repeat():
+    wl = synth.WORKLOADS[2]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=20000)
+    a = _run(g, wl.K, wl.r, wl.q, "median", "fused")
+    b = _run(g, wl.K, wl.r, wl.q, "median", "fused")
+    assert (to_np(a["out"]).view(np.uint32) == to_np(b["out"]).view(np.uint32)).all()
+    assert (to_np(a["bufs"].pair_diff) == to_np(b["bufs"].pair_diff)).all()
+
+
+def test_no_files_leaves_out_untouched():
+    import torch
+    K, r, d = 7, 3, 100
+    g = np.zeros((35, 3, d), dtype=np.float32)
+    gd = torch.from_numpy(g).to(device())
+    bufs = aspis.detect(gd, K, r)
+    res = aspis.CliqueResult()
+    res.success, res.omega, res.n_maximum, res.n_words = 1, 0, 1, 1   # empty honest set
+    out = torch.full((d,), 7.0, device=gd.device)
+    with pytest.raises(aspis.AspisError) as e:
+        aspis.aggregate(gd, K, r, bufs, res, "median", out=out)
+    assert e.value.status == aspis.ERR_NO_FILES
+    torch.cuda.synchronize()
+    assert (to_np(out) == 7.0).all()
+
+
+def test_unaligned_rows_use_scalar_loads():
+    """d not a multiple of 4 and a tensor that starts 4 bytes into a block."""
+    import torch
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = 1001
+    g, _ = synth.generate(wl, s, d=d)
+    ref = oracle.run(g, wl.K, wl.r, wl.q)
+    big = torch.zeros(g.size + 1, dtype=torch.float32, device=device())
+    gd = big[1:].view(g.shape)
+    gd.copy_(torch.from_numpy(g))
+    got = aspis.detect_aggregate(gd, wl.K, wl.r, wl.q)
+    assert_same_floats(to_np(got["out"]), ref["out"])
