@@ -77,6 +77,9 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: run `python -c 'import __graft_entry__ as g; "
                           f"g.build()'` (or python paper_2108_02416_amd/build.py) first")
+    # torch bundles a HIP runtime whose soname equals the system one; it must
+    # be mapped first so that torch and this library share one runtime.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
     L.aspis_num_files.argtypes = [i32, i32]

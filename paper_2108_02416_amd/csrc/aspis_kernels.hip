@@ -15,10 +15,15 @@
 //   median_kernel  Algorithm 1 Case 2 coordinate-wise median: a tile of T
 //                  coordinates x all kept rows is staged in LDS as totalOrder
 //                  keys, then each column's lower median is found by an MSB
-//                  radix select run by G = 256/T lanes per column.
+//                  radix select run by G = BLOCK/T lanes of one wave.
 //   fused_kernel   agree + median in one read: streams all r replicas of a
 //                  tile, compares them, and stages the guessed selection.
 //   mean_kernel    Algorithm 1 Case 1 mean, fp64 accumulation in file order.
+//
+// The tile kernels run one 1024-thread workgroup per CU (16 waves; 512 or
+// 256 threads for the narrow tiles), issue each batch of row loads as a
+// burst before using any of them, and read the LDS tile in batches of eight
+// during the selection, so that neither phase is bound by latency.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -41,39 +46,56 @@ __device__ __forceinline__ uint32_t from_key(uint32_t k) {
     return (k & 0x80000000u) ? (k ^ 0x80000000u) : ~k;
 }
 
-template <int G>
-__device__ __forceinline__ uint32_t group_and(uint32_t v) {
-#pragma unroll
-    for (int o = 1; o < G; o <<= 1) v &= (uint32_t)__shfl_xor((int)v, o, G);
-    return v;
+// Reductions over groups of G consecutive lanes (G a power of two <= 64).
+// Offsets below 16 use DPP row permutations: after the two quad steps every
+// lane of a quad holds the quad's value, and the half-row / row mirrors pair
+// each lane with one lane of the other half.
+enum class Op { And, Or, Add };
+
+template <Op OP>
+__device__ __forceinline__ uint32_t combine(uint32_t a, uint32_t b) {
+    if constexpr (OP == Op::And) return a & b;
+    if constexpr (OP == Op::Or) return a | b;
+    return a + b;
 }
-template <int G>
-__device__ __forceinline__ uint32_t group_or(uint32_t v) {
-#pragma unroll
-    for (int o = 1; o < G; o <<= 1) v |= (uint32_t)__shfl_xor((int)v, o, G);
-    return v;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
-template <int G>
-__device__ __forceinline__ int group_add(int v) {
-#pragma unroll
-    for (int o = 1; o < G; o <<= 1) v += __shfl_xor(v, o, G);
+
+template <int G, Op OP>
+__device__ __forceinline__ uint32_t group_reduce(uint32_t v) {
+    static_assert(G >= 1 && G <= 64 && (G & (G - 1)) == 0, "group size");
+    if constexpr (G >= 2) v = combine<OP>(v, dpp<0xB1>(v));    // quad_perm [1,0,3,2]
+    if constexpr (G >= 4) v = combine<OP>(v, dpp<0x4E>(v));    // quad_perm [2,3,0,1]
+    if constexpr (G >= 8) v = combine<OP>(v, dpp<0x141>(v));   // row_half_mirror
+    if constexpr (G >= 16) v = combine<OP>(v, dpp<0x140>(v));  // row_mirror
+    if constexpr (G >= 32) v = combine<OP>(v, (uint32_t)__shfl_xor((int)v, 16, 64));
+    if constexpr (G >= 64) v = combine<OP>(v, (uint32_t)__shfl_xor((int)v, 32, 64));
     return v;
 }
 
+// Threads per workgroup of the tile kernels for tile width T: 1024 down to
+// 16-wide tiles, then one wave (64 lanes) per column.
+template <int T>
+constexpr int tile_block() { return T >= 16 ? 1024 : 64 * T; }
+
 // LDS layout of a [rows x T] key tile.  Row j lives at j*T; within the row,
-// column c is stored at c ^ swz(j) so that the G lanes working on one column
-// (rows j == g mod G) and the neighbouring columns of a half-wave hit
-// distinct banks.
+// column c is stored at c ^ swz(j % G).  During the selection the G lanes of
+// a column read rows j == g (mod G); the swizzle puts the 32 lanes of every
+// half-wave in 32 distinct banks.
 template <int T>
 __device__ __forceinline__ int tile_swz(int g) {
     static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64, "tile width");
-    if constexpr (T == 4) {
-        return (g >> 3) & 3;                 // 64 lanes per column: 2-way at best
-    } else {
-        const int u = (T >= 32) ? g : g / (32 / T);
-        return u * (T / 8);                  // < T for every g < kBlock / T
-    }
+    constexpr int G = tile_block<T>() / T;
+    if constexpr (T >= 32)
+        return g * (32 / G);                 // G <= 32 here
+    else
+        return (g / (32 / T)) & (T - 1);     // G == 64 here
 }
+
+constexpr int kSelBatch = 8;   // LDS reads in flight per lane
 
 // Lower median (rank floor((n-1)/2)) of each of the T columns of the LDS key
 // tile holding n rows; written to out[k0 + c] for k0 + c < d.
@@ -83,8 +105,9 @@ __device__ __forceinline__ int tile_swz(int g) {
 template <int T>
 __device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0,
                                             int64_t d, float *out) {
-    constexpr int G = kBlock / T;
-    constexpr int STRIDE = G * T;     // words between a lane's rows (= kBlock)
+    constexpr int BLOCK = tile_block<T>();
+    constexpr int G = BLOCK / T;
+    constexpr int STRIDE = G * T;     // words between a lane's rows (= BLOCK)
     const int tid = threadIdx.x;
     const int g = tid % G;
     const int c = tid / G;
@@ -94,41 +117,62 @@ __device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0,
     uint32_t m = (uint32_t)(n - 1) / 2;
 
     uint32_t a = 0xFFFFFFFFu, o = 0u;
-    for (int x = 0; x < cnt; ++x) {
-        const uint32_t key = base[x * STRIDE];
-        a &= key;
-        o |= key;
+    for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
+        uint32_t v[kSelBatch];
+#pragma unroll
+        for (int u = 0; u < kSelBatch; ++u) v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : 0u;
+#pragma unroll
+        for (int u = 0; u < kSelBatch; ++u)
+            if (x0 + u < cnt) {
+                a &= v[u];
+                o |= v[u];
+            }
     }
-    a = group_and<G>(a);
-    o = group_or<G>(o);
+    a = group_reduce<G, Op::And>(a);
+    o = group_reduce<G, Op::Or>(o);
     uint32_t varying = a ^ o;
     while (varying) {
         const uint32_t bit = 1u << (31 - __clz(varying));
-        int z = 0;
-        for (int x = 0; x < cnt; ++x) z += (base[x * STRIDE] & bit) == 0u;
-        z = group_add<G>(z);
+        uint32_t z = 0;
+        for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
+            uint32_t v[kSelBatch];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u)
+                v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : 0xFFFFFFFFu;
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u) z += (v[u] & bit) == 0u;
+        }
+        z = group_reduce<G, Op::Add>(z);
         uint32_t want;
-        if (m < (uint32_t)z) {
+        if (m < z) {
             want = 0u;
         } else {
             want = bit;
-            m -= (uint32_t)z;
+            m -= z;
         }
+        // keep the candidates on the sought side; a batch is read before any
+        // of its slots is overwritten and writes never pass the read point
         int w = 0;
         a = 0xFFFFFFFFu;
         o = 0u;
-        for (int x = 0; x < cnt; ++x) {
-            const uint32_t key = base[x * STRIDE];
-            if ((key & bit) == want) {
-                base[w * STRIDE] = key;
-                ++w;
-                a &= key;
-                o |= key;
-            }
+        const uint32_t reject = want ^ bit;
+        for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
+            uint32_t v[kSelBatch];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u)
+                v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : reject;
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u)
+                if ((v[u] & bit) == want) {
+                    base[w * STRIDE] = v[u];
+                    ++w;
+                    a &= v[u];
+                    o |= v[u];
+                }
         }
         cnt = w;
-        a = group_and<G>(a);
-        o = group_or<G>(o);
+        a = group_reduce<G, Op::And>(a);
+        o = group_reduce<G, Op::Or>(o);
         varying = a ^ o;
     }
     if (g == 0 && k0 + c < d) out[k0 + c] = __uint_as_float(from_key(a));
@@ -314,28 +358,41 @@ __global__ void compare_sel_kernel(const int32_t *a, const int32_t *b, int64_t f
 // ---------------------------------------------------------------------------
 // median of the kept rows
 
+constexpr int kMedianBatch = 8;   // row loads per thread issued as one burst
+
 template <int T, bool VEC>
-__global__ void __launch_bounds__(kBlock)
+__global__ void __launch_bounds__(tile_block<T>())
 median_kernel(const float *__restrict__ g, int64_t d,
               const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
               int64_t ntiles, float *__restrict__ out) {
     extern __shared__ uint32_t tile[];
-    constexpr int G = kBlock / T;
+    constexpr int BLOCK = tile_block<T>();
+    constexpr int G = BLOCK / T;
     constexpr int CPR = T / 4;           // float4 chunks per row segment
-    constexpr int RPI = kBlock / CPR;    // rows filled per sweep
+    constexpr int RPI = BLOCK / CPR;     // rows filled per sweep
     const int n = *n_sel;
     if (n <= 0) return;
     const int tid = threadIdx.x;
     const int cq = tid % CPR, j0 = tid / CPR;
     for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const int64_t k0 = t * T;
-        for (int j = j0; j < n; j += RPI) {
-            const float *row = g + (int64_t)rows[j] * d;
-            uint32_t v[4];
-            load4<VEC>(row, k0 + 4 * cq, d, v);
-            const int sw = tile_swz<T>(j % G);
+        for (int jb = 0; jb < n; jb += RPI * kMedianBatch) {
+            uint32_t v[kMedianBatch][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(v[e]);
+            for (int b = 0; b < kMedianBatch; ++b) {
+                const int j = jb + b * RPI + j0;
+                if (j < n) load4<VEC>(g + (int64_t)rows[j] * d, k0 + 4 * cq, d, v[b]);
+            }
+#pragma unroll
+            for (int b = 0; b < kMedianBatch; ++b) {
+                const int j = jb + b * RPI + j0;
+                if (j < n) {
+                    const int sw = tile_swz<T>(j % G);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        tile[j * T + ((4 * cq + e) ^ sw)] = to_key(v[b][e]);
+                }
+            }
         }
         __syncthreads();
         select_tile<T>(tile, n, k0, d, out);
@@ -346,62 +403,78 @@ median_kernel(const float *__restrict__ g, int64_t d,
 // ---------------------------------------------------------------------------
 // fused agreement + median (one read of all r replicas)
 
+template <int R>
+constexpr int fused_batch() { return R == 3 ? 4 : (R == 5 ? 2 : 1); }
+
 template <int T, int R, bool VEC>
-__global__ void __launch_bounds__(kBlock)
+__global__ void __launch_bounds__(tile_block<T>())
 fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
              const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
              const int32_t *__restrict__ n_sel, int64_t ntiles,
              uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
     extern __shared__ uint32_t smem[];
-    constexpr int G = kBlock / T;
+    constexpr int BLOCK = tile_block<T>();
+    constexpr int G = BLOCK / T;
     constexpr int CPR = T / 4;
-    constexpr int RPI = kBlock / CPR;
+    constexpr int RPI = BLOCK / CPR;
+    constexpr int B = fused_batch<R>();
     const int n = *n_sel;
     uint32_t *tile = smem;
     uint32_t *pd = smem + f * T;         // [f] per-workgroup pair-difference bits
     const int tid = threadIdx.x;
-    for (int64_t i = tid; i < f; i += kBlock) pd[i] = 0u;
+    for (int64_t i = tid; i < f; i += BLOCK) pd[i] = 0u;
     __syncthreads();
     const int cq = tid % CPR, j0 = tid / CPR;
     for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const int64_t k0 = t * T;
-        for (int64_t i = j0; i < f; i += RPI) {
-            const float *rows = g + i * R * d;
-            uint32_t v[R][4];
+        for (int64_t ib = 0; ib < f; ib += (int64_t)RPI * B) {
+            uint32_t v[B][R][4];
 #pragma unroll
-            for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k0 + 4 * cq, d, v[s]);
-            uint32_t diff = 0u;
-            int p = 0;
+            for (int b = 0; b < B; ++b) {
+                const int64_t i = ib + b * RPI + j0;
+                if (i < f) {
+                    const float *rows = g + i * R * d;
 #pragma unroll
-            for (int s = 0; s < R; ++s)
-#pragma unroll
-                for (int u = s + 1; u < R; ++u) {
-                    const uint32_t x = (v[s][0] ^ v[u][0]) | (v[s][1] ^ v[u][1]) |
-                                       (v[s][2] ^ v[u][2]) | (v[s][3] ^ v[u][3]);
-                    diff |= (x != 0u ? 1u : 0u) << p;
-                    ++p;
+                    for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k0 + 4 * cq, d, v[b][s]);
                 }
-            if (diff) atomicOr(&pd[i], diff);
-            const int j = pos[i];
-            if (j >= 0) {
-                const int s_sel = sel[i];
-                uint32_t w[4];
+            }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    w[e] = v[0][e];
+            for (int b = 0; b < B; ++b) {
+                const int64_t i = ib + b * RPI + j0;
+                if (i >= f) continue;
+                uint32_t diff = 0u;
+                int p = 0;
 #pragma unroll
-                    for (int s = 1; s < R; ++s) w[e] = (s_sel == s) ? v[s][e] : w[e];
+                for (int s = 0; s < R; ++s)
+#pragma unroll
+                    for (int u = s + 1; u < R; ++u) {
+                        const uint32_t x = (v[b][s][0] ^ v[b][u][0]) | (v[b][s][1] ^ v[b][u][1]) |
+                                           (v[b][s][2] ^ v[b][u][2]) | (v[b][s][3] ^ v[b][u][3]);
+                        diff |= (x != 0u ? 1u : 0u) << p;
+                        ++p;
+                    }
+                if (diff) atomicOr(&pd[i], diff);
+                const int j = pos[i];
+                if (j >= 0) {
+                    const int s_sel = sel[i];
+                    uint32_t w[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        w[e] = v[b][0][e];
+#pragma unroll
+                        for (int s = 1; s < R; ++s) w[e] = (s_sel == s) ? v[b][s][e] : w[e];
+                    }
+                    const int sw = tile_swz<T>(j % G);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(w[e]);
                 }
-                const int sw = tile_swz<T>(j % G);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(w[e]);
             }
         }
         __syncthreads();
         if (n > 0) select_tile<T>(tile, n, k0, d, out);
         __syncthreads();
     }
-    for (int64_t i = tid; i < f; i += kBlock)
+    for (int64_t i = tid; i < f; i += BLOCK)
         if (pd[i]) atomicOr(&pair_diff[i], pd[i]);
 }
 
@@ -473,6 +546,13 @@ int pick_tile(int64_t rows, int64_t extra_bytes) {
     for (int T : {64, 32, 16, 8, 4})
         if (rows * 4 * (int64_t)T + extra_bytes <= kLdsBytes) return T;
     return 0;
+}
+
+// workgroups per CU that the LDS allows, for the grid of a tile kernel
+int64_t tile_grid(int64_t ntiles, size_t lds) {
+    int per_cu = (int)(kLdsBytes / (int64_t)(lds ? lds : 1));
+    per_cu = per_cu < 1 ? 1 : (per_cu > 2 ? 2 : per_cu);
+    return grid_for(ntiles, (int64_t)num_cus() * per_cu);
 }
 
 }  // namespace
@@ -565,15 +645,15 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)f * 4 * T;
-    const int per_cu = (int)(kLdsBytes / (int64_t)(lds ? lds : 1));
-    const unsigned grid =
-        (unsigned)grid_for(ntiles, (int64_t)num_cus() * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
+    const unsigned grid = (unsigned)tile_grid(ntiles, lds);
     const bool vec = (d % 4 == 0) && aligned16(g);
-#define ASPIS_MED(TT)                                                                      \
-    if (vec)                                                                               \
-        median_kernel<TT, true><<<grid, kBlock, lds, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out); \
-    else                                                                                   \
-        median_kernel<TT, false><<<grid, kBlock, lds, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+#define ASPIS_MED(TT)                                                                        \
+    if (vec)                                                                                 \
+        median_kernel<TT, true><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
+                                                                   ntiles, out);             \
+    else                                                                                     \
+        median_kernel<TT, false><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
+                                                                    ntiles, out);
     switch (T) {
     case 64: ASPIS_MED(64) break;
     case 32: ASPIS_MED(32) break;
@@ -596,17 +676,15 @@ hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Works
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)f * 4 * T + (size_t)f * 4;
-    const int per_cu = (int)(kLdsBytes / (int64_t)lds);
-    const unsigned grid =
-        (unsigned)grid_for(ntiles, (int64_t)num_cus() * (per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu)));
+    const unsigned grid = (unsigned)tile_grid(ntiles, lds);
     const bool vec = (d % 4 == 0) && aligned16(g);
 #define ASPIS_FUSED(TT, RR)                                                                  \
     if (vec)                                                                                 \
-        fused_kernel<TT, RR, true><<<grid, kBlock, lds, s>>>(g, f, d, ws.sel, ws.pos, ws.n_sel, \
-                                                             ntiles, pair_diff, out);        \
+        fused_kernel<TT, RR, true><<<grid, tile_block<TT>(), lds, s>>>(                      \
+            g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                      \
     else                                                                                     \
-        fused_kernel<TT, RR, false><<<grid, kBlock, lds, s>>>(g, f, d, ws.sel, ws.pos,        \
-                                                              ws.n_sel, ntiles, pair_diff, out);
+        fused_kernel<TT, RR, false><<<grid, tile_block<TT>(), lds, s>>>(                     \
+            g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_FUSED_R(TT)                     \
     switch (r) {                              \
     case 3: ASPIS_FUSED(TT, 3) break;         \

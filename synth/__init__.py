@@ -44,6 +44,9 @@ def _load():
     if not os.path.exists(_LIB_PATH):
         from . import build as _b
         _b.build()
+    # torch bundles a HIP runtime whose soname equals the system one; it must
+    # be mapped first so that torch and the GPU fill share one runtime.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(_LIB_PATH)
     P = ctypes.c_void_p
     lib.synth_fill.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
