@@ -81,68 +81,95 @@ __device__ __forceinline__ uint32_t group_reduce(uint32_t v) {
 template <int T>
 constexpr int tile_block() { return T >= 16 ? 1024 : 64 * T; }
 
-// LDS layout of a [rows x T] key tile.  Row j lives at j*T; within the row,
-// column c is stored at c ^ swz(j % G).  During the selection the G lanes of
-// a column read rows j == g (mod G); the swizzle puts the 32 lanes of every
-// half-wave in 32 distinct banks.
-template <int T>
+// LDS layout of a [rows x T] key tile read by G lanes per column.  Row j
+// lives at j*T; within the row, column c is stored at c ^ swz(j % G).  The
+// G lanes of a column read rows j == g (mod G); the swizzle puts the 32
+// lanes of every half-wave in 32 distinct banks.
+template <int T, int G>
 __device__ __forceinline__ int tile_swz(int g) {
     static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64, "tile width");
-    constexpr int G = tile_block<T>() / T;
-    if constexpr (T >= 32)
-        return g * (32 / G);                 // G <= 32 here
-    else
-        return (g / (32 / T)) & (T - 1);     // G == 64 here
+    static_assert(G >= 1 && G <= 64 && (G & (G - 1)) == 0, "lanes per column");
+    if constexpr (T >= 32) {
+        static_assert(G <= 32, "swizzle needs at most 32 lanes per wide column");
+        return g * (32 / G);
+    } else {
+        return (g / (32 / T)) & (T - 1);
+    }
+}
+
+// Store the keys of row j, columns 4cq..4cq+3.
+template <int T, int G>
+__device__ __forceinline__ void put_keys(uint32_t *tile, int j, int cq, const uint32_t k[4]) {
+    const int sw = tile_swz<T, G>(j % G);
+    if constexpr (T >= 32 && (32 / G) % 4 == 0) {
+        // the swizzle keeps each aligned group of four columns together
+        *reinterpret_cast<uint4 *>(&tile[j * T + ((4 * cq) ^ sw)]) = make_uint4(k[0], k[1], k[2], k[3]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = k[e];
+    }
 }
 
 constexpr int kSelBatch = 8;   // LDS reads in flight per lane
 
 // Lower median (rank floor((n-1)/2)) of each of the T columns of the LDS key
-// tile holding n rows; written to out[k0 + c] for k0 + c < d.
+// tile holding n rows, found by the G lanes stid = c*G + g of each column c;
+// written to out[k0 + c] for k0 + c < d.
 // MSB-first radix select: the candidates of a column are split on the
 // highest bit where they still differ, the side holding the sought rank is
-// kept (compacted in place), until all candidates are equal.
-template <int T>
-__device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0,
-                                            int64_t d, float *out) {
-    constexpr int BLOCK = tile_block<T>();
-    constexpr int G = BLOCK / T;
-    constexpr int STRIDE = G * T;     // words between a lane's rows (= BLOCK)
-    const int tid = threadIdx.x;
-    const int g = tid % G;
-    const int c = tid / G;
-    const int col = c ^ tile_swz<T>(g);
-    uint32_t *base = tile + g * T + col;
+// kept (compacted in place), until all candidates are equal.  Lane g owns
+// rows g, g+G, ...; its x-th candidate lives at base[x*STRIDE].
+template <int T, int G>
+__device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0, int64_t d,
+                                            float *out, int stid) {
+    constexpr int STRIDE = G * T;
+    const int g = stid % G;
+    const int c = stid / G;
+    uint32_t *base = tile + g * T + (c ^ tile_swz<T, G>(g));
     int cnt = (n > g) ? (n - g + G - 1) / G : 0;
     uint32_t m = (uint32_t)(n - 1) / 2;
 
-    uint32_t a = 0xFFFFFFFFu, o = 0u;
-    for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
+    // first pass: common bits of the column and the count of sign-clear keys
+    uint32_t a = 0xFFFFFFFFu, o = 0u, z = 0u;
+    int x = 0;
+    for (; x + kSelBatch <= cnt; x += kSelBatch) {
         uint32_t v[kSelBatch];
 #pragma unroll
-        for (int u = 0; u < kSelBatch; ++u) v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : 0u;
+        for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
 #pragma unroll
-        for (int u = 0; u < kSelBatch; ++u)
-            if (x0 + u < cnt) {
-                a &= v[u];
-                o |= v[u];
-            }
+        for (int u = 0; u < kSelBatch; ++u) {
+            a &= v[u];
+            o |= v[u];
+            z += (v[u] >> 31) ^ 1u;
+        }
+    }
+    for (; x < cnt; ++x) {
+        const uint32_t v = base[x * STRIDE];
+        a &= v;
+        o |= v;
+        z += (v >> 31) ^ 1u;
     }
     a = group_reduce<G, Op::And>(a);
     o = group_reduce<G, Op::Or>(o);
+    z = group_reduce<G, Op::Add>(z);
     uint32_t varying = a ^ o;
+    bool have_count = (varying >> 31) != 0u;   // z counts zeros of the top bit
     while (varying) {
         const uint32_t bit = 1u << (31 - __clz(varying));
-        uint32_t z = 0;
-        for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
-            uint32_t v[kSelBatch];
+        if (!have_count) {
+            z = 0u;
+            x = 0;
+            for (; x + kSelBatch <= cnt; x += kSelBatch) {
+                uint32_t v[kSelBatch];
 #pragma unroll
-            for (int u = 0; u < kSelBatch; ++u)
-                v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : 0xFFFFFFFFu;
+                for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
 #pragma unroll
-            for (int u = 0; u < kSelBatch; ++u) z += (v[u] & bit) == 0u;
+                for (int u = 0; u < kSelBatch; ++u) z += (v[u] & bit) == 0u;
+            }
+            for (; x < cnt; ++x) z += (base[x * STRIDE] & bit) == 0u;
+            z = group_reduce<G, Op::Add>(z);
         }
-        z = group_reduce<G, Op::Add>(z);
+        have_count = false;
         uint32_t want;
         if (m < z) {
             want = 0u;
@@ -150,25 +177,34 @@ __device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0,
             want = bit;
             m -= z;
         }
-        // keep the candidates on the sought side; a batch is read before any
-        // of its slots is overwritten and writes never pass the read point
+        // keep the sought side in place: every value is stored at the write
+        // cursor, which advances only for kept values; a batch is read before
+        // any of its slots is overwritten and the cursor never passes the
+        // read point
         int w = 0;
         a = 0xFFFFFFFFu;
         o = 0u;
-        const uint32_t reject = want ^ bit;
-        for (int x0 = 0; x0 < cnt; x0 += kSelBatch) {
+        x = 0;
+        for (; x + kSelBatch <= cnt; x += kSelBatch) {
             uint32_t v[kSelBatch];
 #pragma unroll
-            for (int u = 0; u < kSelBatch; ++u)
-                v[u] = (x0 + u < cnt) ? base[(x0 + u) * STRIDE] : reject;
+            for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
 #pragma unroll
-            for (int u = 0; u < kSelBatch; ++u)
-                if ((v[u] & bit) == want) {
-                    base[w * STRIDE] = v[u];
-                    ++w;
-                    a &= v[u];
-                    o |= v[u];
-                }
+            for (int u = 0; u < kSelBatch; ++u) {
+                const bool keep = (v[u] & bit) == want;
+                base[w * STRIDE] = v[u];
+                w += keep ? 1 : 0;
+                a &= keep ? v[u] : 0xFFFFFFFFu;
+                o |= keep ? v[u] : 0u;
+            }
+        }
+        for (; x < cnt; ++x) {
+            const uint32_t v = base[x * STRIDE];
+            const bool keep = (v & bit) == want;
+            base[w * STRIDE] = v;
+            w += keep ? 1 : 0;
+            a &= keep ? v : 0xFFFFFFFFu;
+            o |= keep ? v : 0u;
         }
         cnt = w;
         a = group_reduce<G, Op::And>(a);
@@ -387,15 +423,15 @@ median_kernel(const float *__restrict__ g, int64_t d,
             for (int b = 0; b < kMedianBatch; ++b) {
                 const int j = jb + b * RPI + j0;
                 if (j < n) {
-                    const int sw = tile_swz<T>(j % G);
+                    uint32_t k[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        tile[j * T + ((4 * cq + e) ^ sw)] = to_key(v[b][e]);
+                    for (int e = 0; e < 4; ++e) k[e] = to_key(v[b][e]);
+                    put_keys<T, G>(tile, j, cq, k);
                 }
             }
         }
         __syncthreads();
-        select_tile<T>(tile, n, k0, d, out);
+        select_tile<T, G>(tile, n, k0, d, out, tid);
         __syncthreads();
     }
 }
@@ -464,17 +500,153 @@ fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
 #pragma unroll
                         for (int s = 1; s < R; ++s) w[e] = (s_sel == s) ? v[b][s][e] : w[e];
                     }
-                    const int sw = tile_swz<T>(j % G);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) tile[j * T + ((4 * cq + e) ^ sw)] = to_key(w[e]);
+                    for (int e = 0; e < 4; ++e) w[e] = to_key(w[e]);
+                    put_keys<T, G>(tile, j, cq, w);
                 }
             }
         }
         __syncthreads();
-        if (n > 0) select_tile<T>(tile, n, k0, d, out);
+        if (n > 0) select_tile<T, G>(tile, n, k0, d, out, tid);
         __syncthreads();
     }
     for (int64_t i = tid; i < f; i += BLOCK)
+        if (pd[i]) atomicOr(&pair_diff[i], pd[i]);
+}
+
+// ---------------------------------------------------------------------------
+// fused agreement + median, warp-specialised: waves 0-7 stream tile t+1 into
+// registers (compare the r replicas, keep the guessed replica's keys) while
+// waves 8-15 run the selection on tile t in LDS; the keys are handed over
+// between two barriers.  The row loads and the selection overlap inside one
+// workgroup, so a single [f x T] tile of LDS per CU is enough.
+
+constexpr int kWsFill = 512;       // threads of the streaming role
+constexpr int kWsSelect = 512;     // threads of the selection role
+
+template <int R, int SW>
+constexpr int ws_batch() { return R == 3 ? (SW > 16 ? 2 : 3) : 1; }
+
+template <int T, int R, int SW>
+__global__ void __launch_bounds__(kWsFill + kWsSelect)
+fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
+                const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
+                const int32_t *__restrict__ n_sel, int64_t ntiles,
+                uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
+    extern __shared__ uint32_t smem[];
+    constexpr int G = kWsSelect / T;     // selection lanes per column
+    constexpr int CPR = T / 4;           // float4 chunks per row segment
+    constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
+    constexpr int B = ws_batch<R, SW>(); // sweeps per burst of loads
+    const int n = *n_sel;
+    uint32_t *tile = smem;
+    uint32_t *pd = smem + f * T;         // [f] per-workgroup pair-difference bits
+    int32_t *ps = reinterpret_cast<int32_t *>(pd + f);   // [f] (tile row << 3) | slot, or -1
+    const int tid = threadIdx.x;
+    for (int64_t i = tid; i < f; i += kWsFill + kWsSelect) {
+        pd[i] = 0u;
+        ps[i] = pos[i] >= 0 ? (pos[i] << 3) | sel[i] : -1;
+    }
+    __syncthreads();
+    // roles are whole waves: waves 0-7 stream, waves 8-15 select; every wave
+    // executes the same number of barriers (1 + 2 per tile)
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (wave < kWsFill / 64) {
+        const int cq = tid % CPR, j0 = tid / CPR;
+        uint32_t keys[SW][4];
+        auto stream_tile = [&](int64_t t) {
+            const bool inside = t * T + 4 * cq < d;
+            const float *base = g + (int64_t)j0 * R * d + t * T + 4 * cq;
+            // an opaque copy of the tile's base address: every row address
+            // below is recomputed from it, instead of the compiler carrying
+            // one incremented pointer per row across tiles (R*SW register
+            // pairs)
+            asm volatile("" : "+v"(base));
+            const int64_t sweep = (int64_t)RPI * R * d;
+#pragma unroll
+            for (int xb = 0; xb < SW; xb += B) {
+                uint32_t v[B][R][4];
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    const int64_t i = j0 + (int64_t)(xb + b) * RPI;
+                    if (xb + b < SW && i < f) {
+                        const float *rows = base + (xb + b) * sweep;
+#pragma unroll
+                        for (int s = 0; s < R; ++s) {
+                            // d % 4 == 0 here, so a chunk is either wholly
+                            // inside the row or wholly past its end (tail tile)
+                            float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
+                            if (inside) q = *reinterpret_cast<const float4 *>(rows + s * d);
+                            v[b][s][0] = __float_as_uint(q.x);
+                            v[b][s][1] = __float_as_uint(q.y);
+                            v[b][s][2] = __float_as_uint(q.z);
+                            v[b][s][3] = __float_as_uint(q.w);
+                        }
+                    }
+                }
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    const int64_t i = j0 + (int64_t)(xb + b) * RPI;
+                    if (xb + b < SW && i < f) {
+                        uint32_t diff = 0u;
+                        int p = 0;
+#pragma unroll
+                        for (int s = 0; s < R; ++s)
+#pragma unroll
+                            for (int u = s + 1; u < R; ++u) {
+                                const uint32_t x = (v[b][s][0] ^ v[b][u][0]) | (v[b][s][1] ^ v[b][u][1]) |
+                                                   (v[b][s][2] ^ v[b][u][2]) | (v[b][s][3] ^ v[b][u][3]);
+                                diff |= (x != 0u ? 1u : 0u) << p;
+                                ++p;
+                            }
+                        if (diff) atomicOr(&pd[i], diff);
+                        const int s_sel = ps[i] & 7;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            uint32_t w = v[b][0][e];
+#pragma unroll
+                            for (int s = 1; s < R; ++s) w = (s_sel == s) ? v[b][s][e] : w;
+                            keys[xb + b][e] = to_key(w);
+                        }
+                    }
+                }
+                // keep each burst's loads together: no scheduling across
+                // bursts, which would hold more loads in registers than fit
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        auto put_tile = [&]() {
+#pragma unroll
+            for (int x = 0; x < SW; ++x) {
+                const int64_t i = j0 + (int64_t)x * RPI;
+                if (i < f) {
+                    const int q = ps[i];
+                    if (q >= 0) put_keys<T, G>(tile, q >> 3, cq, keys[x]);
+                }
+            }
+        };
+        int64_t t = blockIdx.x;
+        if (t < ntiles) {
+            stream_tile(t);
+            put_tile();
+        }
+        __syncthreads();
+        for (; t < ntiles; t += gridDim.x) {
+            const int64_t tn = t + gridDim.x;
+            if (tn < ntiles) stream_tile(tn);
+            __syncthreads();
+            if (tn < ntiles) put_tile();
+            __syncthreads();
+        }
+    } else {
+        __syncthreads();
+        for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+            if (n > 0) select_tile<T, G>(tile, n, t * T, d, out, tid - kWsFill);
+            __syncthreads();
+            __syncthreads();
+        }
+    }
+    for (int64_t i = tid; i < f; i += kWsFill + kWsSelect)
         if (pd[i]) atomicOr(&pair_diff[i], pd[i]);
 }
 
@@ -666,18 +838,71 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     return hipGetLastError();
 }
 
+// Warp-specialised single pass: widest tile (>= 8 columns) whose key block
+// and pair-difference words fit in LDS and whose rows fit the streaming
+// role's register budget (at most 20 sweeps of 512 threads).
+struct WsPlan {
+    int T = 0;
+    int sweeps = 0;
+};
+
+WsPlan ws_plan(int64_t f, int r, bool vec) {
+    WsPlan p;
+    if (r != 3 || !vec) return p;
+    for (int T : {64, 32, 16, 8}) {
+        if (f * 4 * (int64_t)T + f * 8 > kLdsBytes) continue;
+        const int64_t rpi = kWsFill / (T / 4);
+        const int64_t sw = (f + rpi - 1) / rpi;
+        if (sw > 20) continue;
+        p.T = T;
+        p.sweeps = sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : sw <= 16 ? 16 : 20;
+        return p;
+    }
+    return p;
+}
+
 bool fused_supported(int64_t f, int r) {
     return (r == 3 || r == 5 || r == 7) && pick_tile(f, f * 4) != 0;
 }
 
 hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Workspace &ws,
                         uint32_t *pair_diff, float *out, hipStream_t s) {
+    const bool vec = (d % 4 == 0) && aligned16(g);
+    const WsPlan plan = ws_plan(f, r, vec);
+    if (plan.T != 0) {
+        const int T = plan.T;
+        const int64_t ntiles = (d + T - 1) / T;
+        const size_t lds = (size_t)f * 4 * T + (size_t)f * 8;
+        const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
+#define ASPIS_WS(TT, SWW)                                                                        \
+    fused_ws_kernel<TT, 3, SWW><<<grid, kWsFill + kWsSelect, lds, s>>>(                          \
+        g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+#define ASPIS_WS_T(TT)                             \
+    switch (plan.sweeps) {                         \
+    case 2: ASPIS_WS(TT, 2) break;                 \
+    case 4: ASPIS_WS(TT, 4) break;                 \
+    case 8: ASPIS_WS(TT, 8) break;                 \
+    case 12: ASPIS_WS(TT, 12) break;               \
+    case 16: ASPIS_WS(TT, 16) break;               \
+    case 20: ASPIS_WS(TT, 20) break;               \
+    default: return hipErrorInvalidValue;          \
+    }
+        switch (T) {
+        case 64: ASPIS_WS_T(64) break;
+        case 32: ASPIS_WS_T(32) break;
+        case 16: ASPIS_WS_T(16) break;
+        case 8: ASPIS_WS_T(8) break;
+        default: return hipErrorInvalidValue;
+        }
+#undef ASPIS_WS_T
+#undef ASPIS_WS
+        return hipGetLastError();
+    }
     const int T = pick_tile(f, f * 4);
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)f * 4 * T + (size_t)f * 4;
     const unsigned grid = (unsigned)tile_grid(ntiles, lds);
-    const bool vec = (d % 4 == 0) && aligned16(g);
 #define ASPIS_FUSED(TT, RR)                                                                  \
     if (vec)                                                                                 \
         fused_kernel<TT, RR, true><<<grid, tile_block<TT>(), lds, s>>>(                      \

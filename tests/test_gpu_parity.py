@@ -44,16 +44,21 @@ def _check(g, K, r, q, mode, path, nan_equal=False):
     return got, ref
 
 
+# d per workload: odd (scalar loads), and a multiple of 4 whose last tile is
+# ragged (vector loads, the warp-specialised single pass)
 _D = {1: 4099, 2: 2053, 3: 1543, 4: 523, 5: 389}
+_D4 = {1: 4100, 2: 2056, 3: 1548, 4: 524, 5: 392}
 
 
 @pytest.mark.parametrize("path", ["fused", "two_pass", "entry_points"])
 @pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
-def test_workloads_small(idx, path):
+@pytest.mark.parametrize("dmap", ["odd", "mult4"])
+def test_workloads_small(idx, path, dmap):
     wl = synth.WORKLOADS[idx]
+    d = (_D if dmap == "odd" else _D4)[idx]
     s = oracle.assign(wl.K, wl.r)
-    g, _ = synth.generate(wl, s, d=_D[idx])
-    print(f"workload {idx} d={_D[idx]} path={path}", flush=True)
+    g, _ = synth.generate(wl, s, d=d)
+    print(f"workload {idx} d={d} path={path}", flush=True)
     _check(g, wl.K, wl.r, wl.q, "median", path)
 
 
@@ -78,7 +83,8 @@ def _random_case(seed: int):
     r = int(rng.choice([3, 3, 5, 7]))
     K = int(rng.integers(max(r, 3), 13 if r < 7 else 10))
     q = int(rng.integers(0, (K + 1) // 2))
-    d = int(rng.choice([1, 2, 3, 5, 17, 63, 64, 65, 255, 257, 1000, 4097]))
+    d = int(rng.choice([1, 2, 3, 4, 5, 8, 17, 60, 63, 64, 65, 68, 255, 256, 257, 1000, 4096,
+                        4097]))
     f = comb(K, r)
     # per file, a random partition of the slots into classes of equal replicas
     g = np.empty((f, r, d), dtype=np.float32)
@@ -105,7 +111,7 @@ def _random_case(seed: int):
     return g, K, r, q
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(32))
 def test_random_properties(seed):
     g, K, r, q = _random_case(seed)
     print(f"seed={seed} K={K} r={r} q={q} d={g.shape[2]}", flush=True)
@@ -114,7 +120,8 @@ def test_random_properties(seed):
     _check(g, K, r, q, "mean", "two_pass", nan_equal=True)
 
 
-@pytest.mark.parametrize("K,r,d", [(26, 3, 301), (32, 3, 97), (9, 7, 333), (13, 5, 129)])
+@pytest.mark.parametrize("K,r,d", [(26, 3, 301), (32, 3, 97), (9, 7, 333), (13, 5, 129),
+                                   (26, 3, 300), (32, 3, 96), (29, 3, 200), (9, 7, 332)])
 def test_tile_widths(K, r, d):
     """f = 2600 (8-wide tiles), 4960 (4-wide), r = 5 and 7."""
     q = (K - 1) // 2 - 1
