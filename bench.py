@@ -78,6 +78,22 @@ def cpu_baseline(wl, role, worker, sample_coords: int, gpu_out, gpu_sel):
             same_out)
 
 
+def copy_probe(torch, aspis, dev, nbytes: int = 1 << 32) -> int:
+    """Kernels of known traffic for scaling the FETCH_SIZE / WRITE_SIZE
+    counters: an elementwise negation (reads and writes nbytes) and the
+    library's read probe (reads nbytes)."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+        aspis.read_probe(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3,
+                      "copy_kernel": "torch.neg (reads and writes copy_probe_bytes)",
+                      "read_kernel": "read_probe_kernel (reads copy_probe_bytes)"}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,8 +102,11 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--seed", type=int, default=428)
     ap.add_argument("--two-pass", action="store_true", help="force the two-pass path")
-    ap.add_argument("--cpu-sample", type=int, default=1 << 18,
+    ap.add_argument("--cpu-sample", type=int, default=1 << 20,
                     help="coordinates of the oracle's CPU-baseline sample (0 = skip)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="instead of the step, run a plain copy kernel and the read probe "
+                         "over 4 GiB (the reference sizes for HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported",
@@ -104,6 +123,8 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     dev = torch.device("cuda:0")
+    if args.copy_probe:
+        return copy_probe(torch, aspis, dev)
     wl = synth.WORKLOADS[args.workload]
     K, r, q, d, f = wl.K, wl.r, wl.q, wl.d, wl.f
     subsets = aspis.assign(K, r)

@@ -129,8 +129,9 @@ typedef struct {
 aspis_status aspis_clique(const uint64_t *disagree_rows, int32_t K, int32_t q,
                           aspis_clique_result *res);
 
-/* Bytes of workspace aspis_aggregate and aspis_detect_aggregate need:
- * f*(4+4+4) + 256, rounded up to 256. 0 on invalid arguments. */
+/* Bytes of workspace aspis_aggregate and aspis_detect_aggregate need: four
+ * int32 [f] arrays, each rounded up to 256 bytes, plus 256 bytes of
+ * counters.  0 on invalid arguments. */
 size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d);
 
 /* Algorithm 1, aggregation.  Selection: on success (Case 1) file i keeps
