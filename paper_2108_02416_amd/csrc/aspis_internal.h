@@ -13,8 +13,14 @@ namespace aspis {
 constexpr int kBlock = 256;                 // threads per workgroup
 constexpr int64_t kLdsBytes = 160 * 1024;   // LDS per CU on gfx950
 
+// The selection keeps a histogram block of kHistStride words per column
+// (128 buckets, an overflow bucket, padding) next to the key tile.
+constexpr int kHistBuckets = 128;
+constexpr int kHistStride = 132;
+constexpr int64_t hist_bytes(int T) { return (int64_t)T * kHistStride * 4; }
+
 // Largest number of kept files the LDS-tiled median supports for tile T.
-inline int64_t median_capacity(int T) { return kLdsBytes / (4 * (int64_t)T); }
+inline int64_t median_capacity(int T) { return (kLdsBytes - hist_bytes(T)) / (4 * (int64_t)T); }
 
 // Workspace layout (byte offsets) for f files.
 struct Workspace {

@@ -50,12 +50,13 @@ __device__ __forceinline__ uint32_t from_key(uint32_t k) {
 // Offsets below 16 use DPP row permutations: after the two quad steps every
 // lane of a quad holds the quad's value, and the half-row / row mirrors pair
 // each lane with one lane of the other half.
-enum class Op { And, Or, Add };
+enum class Op { And, Or, Add, Max };
 
 template <Op OP>
 __device__ __forceinline__ uint32_t combine(uint32_t a, uint32_t b) {
     if constexpr (OP == Op::And) return a & b;
     if constexpr (OP == Op::Or) return a | b;
+    if constexpr (OP == Op::Max) return a > b ? a : b;
     return a + b;
 }
 
@@ -73,6 +74,27 @@ __device__ __forceinline__ uint32_t group_reduce(uint32_t v) {
     if constexpr (G >= 16) v = combine<OP>(v, dpp<0x140>(v));  // row_mirror
     if constexpr (G >= 32) v = combine<OP>(v, (uint32_t)__shfl_xor((int)v, 16, 64));
     if constexpr (G >= 64) v = combine<OP>(v, (uint32_t)__shfl_xor((int)v, 32, 64));
+    return v;
+}
+
+// Inclusive prefix sum over groups of G consecutive lanes; g = lane index
+// within the group.  A group inside one 16-lane row shifts with DPP row_shr;
+// row_shr does not cross rows, so wider groups shift through ds_bpermute.
+template <int G>
+__device__ __forceinline__ uint32_t group_scan(uint32_t v, int g) {
+#pragma unroll
+    for (int k = 1; k < G; k <<= 1) {
+        uint32_t y;
+        if constexpr (G <= 16) {
+            if (k == 1) y = dpp<0x111>(v);
+            else if (k == 2) y = dpp<0x112>(v);
+            else if (k == 4) y = dpp<0x114>(v);
+            else y = dpp<0x118>(v);
+        } else {
+            y = (uint32_t)__shfl_up((int)v, k, 64);
+        }
+        v += (g >= k) ? y : 0u;
+    }
     return v;
 }
 
@@ -112,61 +134,189 @@ __device__ __forceinline__ void put_keys(uint32_t *tile, int j, int cq, const ui
 
 constexpr int kSelBatch = 8;   // LDS reads in flight per lane
 
-// Lower median (rank floor((n-1)/2)) of each of the T columns of the LDS key
-// tile holding n rows, found by the G lanes stid = c*G + g of each column c;
-// written to out[k0 + c] for k0 + c < d.
-// MSB-first radix select: the candidates of a column are split on the
-// highest bit where they still differ, the side holding the sought rank is
-// kept (compacted in place), until all candidates are equal.  Lane g owns
-// rows g, g+G, ...; its x-th candidate lives at base[x*STRIDE].
-template <int T, int G>
-__device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0, int64_t d,
-                                            float *out, int stid) {
-    constexpr int STRIDE = G * T;
-    const int g = stid % G;
-    const int c = stid / G;
-    uint32_t *base = tile + g * T + (c ^ tile_swz<T, G>(g));
-    int cnt = (n > g) ? (n - g + G - 1) / G : 0;
-    uint32_t m = (uint32_t)(n - 1) / 2;
+// Per-column histogram of the selection (kHistBuckets buckets plus one
+// overflow bucket); the column stride of kHistStride words keeps each
+// column's bucket block 16-byte aligned and puts equal buckets of
+// neighbouring columns in different banks.
+constexpr int kHistWindow = 7;   // key bits resolved by one histogram round
+static_assert(kHistBuckets == 1 << kHistWindow && kHistStride > kHistBuckets, "histogram");
 
-    // first pass: common bits of the column and the count of sign-clear keys
-    uint32_t a = 0xFFFFFFFFu, o = 0u, z = 0u;
+__host__ __device__ constexpr int64_t hist_words(int T) { return (int64_t)T * kHistStride; }
+
+// One pass over a lane's candidates, in batches of kSelBatch LDS reads.
+template <int STRIDE, typename F>
+__device__ __forceinline__ void for_each_candidate(const uint32_t *base, int cnt, F &&fn) {
     int x = 0;
     for (; x + kSelBatch <= cnt; x += kSelBatch) {
         uint32_t v[kSelBatch];
 #pragma unroll
         for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
 #pragma unroll
+        for (int u = 0; u < kSelBatch; ++u) fn(v[u]);
+    }
+    for (; x < cnt; ++x) fn(base[x * STRIDE]);
+}
+
+// In-place compaction of a lane's candidates: keeps the values for which
+// keep(v) holds, in order.  Every value is stored at the write cursor, which
+// advances only for kept values; a batch is read before any of its slots is
+// overwritten and the cursor never passes the read point.  Returns the
+// number kept.
+template <int STRIDE, typename F>
+__device__ __forceinline__ int compact(uint32_t *base, int cnt, F &&keep) {
+    int w = 0, x = 0;
+    for (; x + kSelBatch <= cnt; x += kSelBatch) {
+        uint32_t v[kSelBatch];
+#pragma unroll
+        for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
+#pragma unroll
         for (int u = 0; u < kSelBatch; ++u) {
-            a &= v[u];
-            o |= v[u];
-            z += (v[u] >> 31) ^ 1u;
+            base[w * STRIDE] = v[u];
+            w += keep(v[u]) ? 1 : 0;
         }
     }
     for (; x < cnt; ++x) {
         const uint32_t v = base[x * STRIDE];
-        a &= v;
-        o |= v;
-        z += (v >> 31) ^ 1u;
+        base[w * STRIDE] = v;
+        w += keep(v) ? 1 : 0;
     }
-    a = group_reduce<G, Op::And>(a);
-    o = group_reduce<G, Op::Or>(o);
-    z = group_reduce<G, Op::Add>(z);
-    uint32_t varying = a ^ o;
-    bool have_count = (varying >> 31) != 0u;   // z counts zeros of the top bit
-    while (varying) {
+    return w;
+}
+
+// Lower median (rank floor((n-1)/2)) of each of the T columns of the LDS key
+// tile holding n rows, found by the G lanes stid = c*G + g of each column c;
+// written to out[k0 + c] for k0 + c < d.  hist: the workgroup's histogram
+// block (hist_words(T) words, zero on entry; left zero on exit except for
+// the overflow buckets).
+//
+// Exact selection on the keys in two stages:
+//  1. histogram rounds while many candidates remain: the bits above the
+//     highest bit where the candidates differ are common to all of them, so
+//     the next kHistWindow bits below it split the candidates into ordered
+//     buckets; an LDS histogram and a prefix scan over the buckets give the
+//     bucket holding the sought rank, and only its members are kept
+//     (compacted in place).  The first round decides the sign from the
+//     count of sign-clear keys and works on the magnitude bits (the keys of
+//     negative values hold them complemented); keys of the other sign land
+//     in the overflow bucket or past every bucket of the sought sign.
+//  2. bitwise MSB radix select on the few survivors: split on the highest
+//     differing bit, keep the side holding the rank, until all are equal.
+// Lane g owns rows g, g+G, ...; its x-th candidate lives at base[x*STRIDE].
+template <int T, int G>
+__device__ __forceinline__ void select_tile(uint32_t *tile, uint32_t *hist, int n, int64_t k0,
+                                            int64_t d, float *out, int stid) {
+    constexpr int STRIDE = G * T;
+    constexpr int BPL = kHistBuckets / G;   // buckets scanned per lane
+    static_assert(BPL >= 2 && BPL % 2 == 0, "buckets per lane");
+    const int g = stid % G;
+    const int c = stid / G;
+    uint32_t *base = tile + g * T + (c ^ tile_swz<T, G>(g));
+    uint32_t *hcol = hist + c * kHistStride;
+    int cnt = (n > g) ? (n - g + G - 1) / G : 0;
+    int total = n;
+    uint32_t m = (uint32_t)(n - 1) / 2;
+
+    // first pass: common magnitude bits and the count of sign-clear keys
+    uint32_t am = 0xFFFFFFFFu, om = 0u, z = 0u;
+    for_each_candidate<STRIDE>(base, cnt, [&](uint32_t v) {
+        const uint32_t mag = (v ^ ~(uint32_t)((int32_t)v >> 31)) & 0x7FFFFFFFu;
+        am &= mag;
+        om |= mag;
+        z += v >> 31;
+    });
+    am = group_reduce<G, Op::And>(am);
+    om = group_reduce<G, Op::Or>(om);
+    z = (uint32_t)total - group_reduce<G, Op::Add>(z);   // keys with the top bit clear
+
+    auto and_or = [&](uint32_t &a, uint32_t &o) {
+        a = 0xFFFFFFFFu;
+        o = 0u;
+        for_each_candidate<STRIDE>(base, cnt, [&](uint32_t v) {
+            a &= v;
+            o |= v;
+        });
+        a = group_reduce<G, Op::And>(a);
+        o = group_reduce<G, Op::Or>(o);
+    };
+    // one histogram round over the candidates whose keys lie in
+    // [bias, bias + 2^(hb+1)); keeps the bucket holding rank m
+    auto hist_round = [&](uint32_t bias, int hb) {
+        const int sh = hb >= kHistWindow - 1 ? hb - (kHistWindow - 1) : 0;
+        for_each_candidate<STRIDE>(base, cnt, [&](uint32_t v) {
+            const uint32_t b = min((v - bias) >> sh, (uint32_t)kHistBuckets);
+            atomicAdd(&hcol[b], 1u);
+        });
+        // bucket holding rank m: B = number of buckets whose inclusive
+        // prefix count is <= m, below = the largest such prefix
+        uint32_t h[BPL];
+#pragma unroll
+        for (int q = 0; q < BPL; q += 2) {
+            const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[g * BPL + q]);
+            h[q] = w2.x;
+            h[q + 1] = w2.y;
+        }
+#pragma unroll
+        for (int q = 0; q < BPL; q += 2)
+            *reinterpret_cast<uint2 *>(&hcol[g * BPL + q]) = make_uint2(0u, 0u);
+        uint32_t tot = 0u;
+#pragma unroll
+        for (int q = 0; q < BPL; ++q) tot += h[q];
+        uint32_t run = group_scan<G>(tot, g) - tot;
+        uint32_t le = 0u, below = 0u;
+#pragma unroll
+        for (int q = 0; q < BPL; ++q) {
+            run += h[q];
+            const bool ok = run <= m;
+            le += ok ? 1u : 0u;
+            below = ok ? run : below;
+        }
+        le = group_reduce<G, Op::Add>(le);
+        below = group_reduce<G, Op::Max>(below);
+        m -= below;
+        const uint32_t lo = bias + (le << sh);
+        const uint32_t width = 1u << sh;
+        cnt = compact<STRIDE>(base, cnt, [&](uint32_t v) { return v - lo < width; });
+        total = (int)group_reduce<G, Op::Add>((uint32_t)cnt);
+    };
+
+    uint32_t a, o, varying;
+    bool have_count = false;
+    if (total > 2 * G) {
+        uint32_t sgn = 0x80000000u;
+        if (m < z) sgn = 0u;
+        else m -= z;
+        const uint32_t vm = am ^ om;
+        if (vm == 0u) {   // every candidate has the same magnitude
+            a = sgn ? (0x80000000u | am) : (~am & 0x7FFFFFFFu);
+            varying = 0u;
+        } else {
+            const int hb = 31 - __clz(vm);
+            const uint32_t hi = 0x7FFFFFFFu & ~((2u << hb) - 1u);
+            hist_round(sgn ? (0x80000000u | (am & hi)) : (~am & hi), hb);
+            and_or(a, o);
+            varying = a ^ o;
+            // the sign is settled now; every round settles the bits from the
+            // highest differing one down to the window's lowest, so the next
+            // round starts strictly lower (at most 31 / kHistWindow more)
+            for (int round = 0; varying != 0u && total > 2 * G && round < 5; ++round) {
+                const int hb2 = 31 - __clz(varying);
+                hist_round(a & ~((2u << hb2) - 1u), hb2);
+                and_or(a, o);
+                varying = a ^ o;
+            }
+        }
+    } else {
+        and_or(a, o);
+        varying = a ^ o;
+        have_count = (varying >> 31) != 0u;   // z counts zeros of the top bit
+    }
+
+    // each step settles the highest differing bit: at most 32 steps
+    for (int step = 0; varying != 0u && step < 32; ++step) {
         const uint32_t bit = 1u << (31 - __clz(varying));
         if (!have_count) {
             z = 0u;
-            x = 0;
-            for (; x + kSelBatch <= cnt; x += kSelBatch) {
-                uint32_t v[kSelBatch];
-#pragma unroll
-                for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
-#pragma unroll
-                for (int u = 0; u < kSelBatch; ++u) z += (v[u] & bit) == 0u;
-            }
-            for (; x < cnt; ++x) z += (base[x * STRIDE] & bit) == 0u;
+            for_each_candidate<STRIDE>(base, cnt, [&](uint32_t v) { z += (v & bit) == 0u; });
             z = group_reduce<G, Op::Add>(z);
         }
         have_count = false;
@@ -177,38 +327,8 @@ __device__ __forceinline__ void select_tile(uint32_t *tile, int n, int64_t k0, i
             want = bit;
             m -= z;
         }
-        // keep the sought side in place: every value is stored at the write
-        // cursor, which advances only for kept values; a batch is read before
-        // any of its slots is overwritten and the cursor never passes the
-        // read point
-        int w = 0;
-        a = 0xFFFFFFFFu;
-        o = 0u;
-        x = 0;
-        for (; x + kSelBatch <= cnt; x += kSelBatch) {
-            uint32_t v[kSelBatch];
-#pragma unroll
-            for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
-#pragma unroll
-            for (int u = 0; u < kSelBatch; ++u) {
-                const bool keep = (v[u] & bit) == want;
-                base[w * STRIDE] = v[u];
-                w += keep ? 1 : 0;
-                a &= keep ? v[u] : 0xFFFFFFFFu;
-                o |= keep ? v[u] : 0u;
-            }
-        }
-        for (; x < cnt; ++x) {
-            const uint32_t v = base[x * STRIDE];
-            const bool keep = (v & bit) == want;
-            base[w * STRIDE] = v;
-            w += keep ? 1 : 0;
-            a &= keep ? v : 0xFFFFFFFFu;
-            o |= keep ? v : 0u;
-        }
-        cnt = w;
-        a = group_reduce<G, Op::And>(a);
-        o = group_reduce<G, Op::Or>(o);
+        cnt = compact<STRIDE>(base, cnt, [&](uint32_t v) { return (v & bit) == want; });
+        and_or(a, o);
         varying = a ^ o;
     }
     if (g == 0 && k0 + c < d) out[k0 + c] = __uint_as_float(from_key(a));
@@ -401,14 +521,17 @@ __global__ void __launch_bounds__(tile_block<T>())
 median_kernel(const float *__restrict__ g, int64_t d,
               const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
               int64_t ntiles, float *__restrict__ out) {
-    extern __shared__ uint32_t tile[];
+    extern __shared__ uint32_t smem[];
     constexpr int BLOCK = tile_block<T>();
+    uint32_t *hist = smem;
+    uint32_t *tile = smem + hist_words(T);
     constexpr int G = BLOCK / T;
     constexpr int CPR = T / 4;           // float4 chunks per row segment
     constexpr int RPI = BLOCK / CPR;     // rows filled per sweep
     const int n = *n_sel;
     if (n <= 0) return;
     const int tid = threadIdx.x;
+    for (int i = tid; i < hist_words(T); i += BLOCK) hist[i] = 0u;
     const int cq = tid % CPR, j0 = tid / CPR;
     for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const int64_t k0 = t * T;
@@ -431,7 +554,7 @@ median_kernel(const float *__restrict__ g, int64_t d,
             }
         }
         __syncthreads();
-        select_tile<T, G>(tile, n, k0, d, out, tid);
+        select_tile<T, G>(tile, hist, n, k0, d, out, tid);
         __syncthreads();
     }
 }
@@ -455,10 +578,12 @@ fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
     constexpr int RPI = BLOCK / CPR;
     constexpr int B = fused_batch<R>();
     const int n = *n_sel;
-    uint32_t *tile = smem;
-    uint32_t *pd = smem + f * T;         // [f] per-workgroup pair-difference bits
+    uint32_t *hist = smem;
+    uint32_t *tile = smem + hist_words(T);
+    uint32_t *pd = tile + f * T;         // [f] per-workgroup pair-difference bits
     const int tid = threadIdx.x;
     for (int64_t i = tid; i < f; i += BLOCK) pd[i] = 0u;
+    for (int i = tid; i < hist_words(T); i += BLOCK) hist[i] = 0u;
     __syncthreads();
     const int cq = tid % CPR, j0 = tid / CPR;
     for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -507,7 +632,7 @@ fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
             }
         }
         __syncthreads();
-        if (n > 0) select_tile<T, G>(tile, n, k0, d, out, tid);
+        if (n > 0) select_tile<T, G>(tile, hist, n, k0, d, out, tid);
         __syncthreads();
     }
     for (int64_t i = tid; i < f; i += BLOCK)
@@ -539,14 +664,16 @@ fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
     constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
     constexpr int B = ws_batch<R, SW>(); // sweeps per burst of loads
     const int n = *n_sel;
-    uint32_t *tile = smem;
-    uint32_t *pd = smem + f * T;         // [f] per-workgroup pair-difference bits
+    uint32_t *hist = smem;               // selection histograms
+    uint32_t *tile = smem + hist_words(T);
+    uint32_t *pd = tile + f * T;         // [f] per-workgroup pair-difference bits
     int32_t *ps = reinterpret_cast<int32_t *>(pd + f);   // [f] (tile row << 3) | slot, or -1
     const int tid = threadIdx.x;
     for (int64_t i = tid; i < f; i += kWsFill + kWsSelect) {
         pd[i] = 0u;
         ps[i] = pos[i] >= 0 ? (pos[i] << 3) | sel[i] : -1;
     }
+    for (int i = tid; i < hist_words(T); i += kWsFill + kWsSelect) hist[i] = 0u;
     __syncthreads();
     // roles are whole waves: waves 0-7 stream, waves 8-15 select; every wave
     // executes the same number of barriers (1 + 2 per tile)
@@ -641,7 +768,7 @@ fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
     } else {
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (n > 0) select_tile<T, G>(tile, n, t * T, d, out, tid - kWsFill);
+            if (n > 0) select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
             __syncthreads();
             __syncthreads();
         }
@@ -716,7 +843,7 @@ int64_t grid_for(int64_t work, int64_t cap) { return work < cap ? (work < 1 ? 1 
 // widest tile T whose [rows x T] key block (plus extra bytes) fits in LDS
 int pick_tile(int64_t rows, int64_t extra_bytes) {
     for (int T : {64, 32, 16, 8, 4})
-        if (rows * 4 * (int64_t)T + extra_bytes <= kLdsBytes) return T;
+        if (rows * 4 * (int64_t)T + hist_words(T) * 4 + extra_bytes <= kLdsBytes) return T;
     return 0;
 }
 
@@ -816,7 +943,7 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     const int T = pick_tile(f, 0);
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
-    const size_t lds = (size_t)f * 4 * T;
+    const size_t lds = (size_t)(f * 4 * T + hist_words(T) * 4);
     const unsigned grid = (unsigned)tile_grid(ntiles, lds);
     const bool vec = (d % 4 == 0) && aligned16(g);
 #define ASPIS_MED(TT)                                                                        \
@@ -850,7 +977,7 @@ WsPlan ws_plan(int64_t f, int r, bool vec) {
     WsPlan p;
     if (r != 3 || !vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (f * 4 * (int64_t)T + f * 8 > kLdsBytes) continue;
+        if (f * 4 * (int64_t)T + f * 8 + hist_words(T) * 4 > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         if (sw > 20) continue;
@@ -872,7 +999,7 @@ hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Works
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)f * 4 * T + (size_t)f * 8;
+        const size_t lds = (size_t)(f * 4 * T + f * 8 + hist_words(T) * 4);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
 #define ASPIS_WS(TT, SWW)                                                                        \
     fused_ws_kernel<TT, 3, SWW><<<grid, kWsFill + kWsSelect, lds, s>>>(                          \
@@ -901,7 +1028,7 @@ hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Works
     const int T = pick_tile(f, f * 4);
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
-    const size_t lds = (size_t)f * 4 * T + (size_t)f * 4;
+    const size_t lds = (size_t)(f * 4 * T + f * 4 + hist_words(T) * 4);
     const unsigned grid = (unsigned)tile_grid(ntiles, lds);
 #define ASPIS_FUSED(TT, RR)                                                                  \
     if (vec)                                                                                 \
