@@ -649,8 +649,10 @@ fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
 constexpr int kWsFill = 512;       // threads of the streaming role
 constexpr int kWsSelect = 512;     // threads of the selection role
 
+// sweeps per burst of loads: as many as the streaming role's registers hold
+// next to the tile's keys (SW x 4 registers)
 template <int R, int SW>
-constexpr int ws_batch() { return R == 3 ? (SW > 16 ? 2 : 3) : 1; }
+constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
 
 template <int T, int R, int SW>
 __global__ void __launch_bounds__(kWsFill + kWsSelect)
@@ -680,87 +682,105 @@ fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if (wave < kWsFill / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
+        const int64_t sweep = (int64_t)RPI * R * d;   // elements between sweeps
         uint32_t keys[SW][4];
-        auto stream_tile = [&](int64_t t) {
-            const bool inside = t * T + 4 * cq < d;
-            const float *base = g + (int64_t)j0 * R * d + t * T + 4 * cq;
-            // an opaque copy of the tile's base address: every row address
-            // below is recomputed from it, instead of the compiler carrying
-            // one incremented pointer per row across tiles (R*SW register
-            // pairs)
-            asm volatile("" : "+v"(base));
-            const int64_t sweep = (int64_t)RPI * R * d;
+        // the r replica chunks of one sweep, kept in registers (a value
+        // type, so that no per-lane indexing can turn it into memory)
+        struct Chunks {
+            uint4 q[R];
+        };
+        // issue the row loads of sweep x of tile t.  Every load is in bounds
+        // and unconditional: a lane past the end of the rows (tail tile;
+        // d % 4 == 0) reads the last chunk of its row instead, and a lane
+        // past the last file reads file 0; proc_sweep ignores files past the
+        // last, and a repeated chunk changes neither the agreement bits nor
+        // any written median.
+        auto load_sweep = [&](int64_t t, int x) __attribute__((always_inline)) {
+            const int64_t col = min(t * T + 4 * cq, d - 4);
+            const float *base = g + (int64_t)j0 * R * d + col;
+            int lim = (int)(f - j0);   // sweeps x with x * RPI < lim hold a file
+            // opaque copies of the tile's base address and of the limit:
+            // every row address and check below is recomputed from them,
+            // instead of the compiler carrying one pointer and one lane mask
+            // per sweep across tiles
+            asm volatile("" : "+v"(base), "+v"(lim));
+            const float *rows = (x * RPI < lim) ? base + x * sweep : g + col;
+            Chunks c;
 #pragma unroll
-            for (int xb = 0; xb < SW; xb += B) {
-                uint32_t v[B][R][4];
+            for (int s = 0; s < R; ++s) c.q[s] = *reinterpret_cast<const uint4 *>(rows + s * d);
+            return c;
+        };
+        // compare the replicas of sweep x and keep the guessed replica's keys
+        auto proc_sweep = [&](int x, Chunks c) __attribute__((always_inline)) {
+            const int i = j0 + x * RPI;   // f <= C(64,3) here
+            if (i < f) {
+                uint32_t diff = 0u;
+                int p = 0;
 #pragma unroll
-                for (int b = 0; b < B; ++b) {
-                    const int64_t i = j0 + (int64_t)(xb + b) * RPI;
-                    if (xb + b < SW && i < f) {
-                        const float *rows = base + (xb + b) * sweep;
+                for (int s = 0; s < R; ++s)
 #pragma unroll
-                        for (int s = 0; s < R; ++s) {
-                            // d % 4 == 0 here, so a chunk is either wholly
-                            // inside the row or wholly past its end (tail tile)
-                            float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-                            if (inside) q = *reinterpret_cast<const float4 *>(rows + s * d);
-                            v[b][s][0] = __float_as_uint(q.x);
-                            v[b][s][1] = __float_as_uint(q.y);
-                            v[b][s][2] = __float_as_uint(q.z);
-                            v[b][s][3] = __float_as_uint(q.w);
-                        }
+                    for (int u = s + 1; u < R; ++u) {
+                        const uint32_t y = (c.q[s].x ^ c.q[u].x) | (c.q[s].y ^ c.q[u].y) |
+                                           (c.q[s].z ^ c.q[u].z) | (c.q[s].w ^ c.q[u].w);
+                        diff |= (y != 0u ? 1u : 0u) << p;
+                        ++p;
                     }
-                }
+                if (diff) atomicOr(&pd[i], diff);
+                const int s_sel = ps[i] & 7;
+                uint4 w = c.q[0];
 #pragma unroll
-                for (int b = 0; b < B; ++b) {
-                    const int64_t i = j0 + (int64_t)(xb + b) * RPI;
-                    if (xb + b < SW && i < f) {
-                        uint32_t diff = 0u;
-                        int p = 0;
+                for (int s = 1; s < R; ++s)
+                    if (s_sel == s) w = c.q[s];
+                keys[x][0] = to_key(w.x);
+                keys[x][1] = to_key(w.y);
+                keys[x][2] = to_key(w.z);
+                keys[x][3] = to_key(w.w);
+            }
+        };
+        Chunks c0;   // sweep 0 of the next tile, loaded early
+        // the rest of tile t, whose sweep 0 is already in c0; the other
+        // sweeps go in bursts of B, all loads of a burst issued first
+        auto stream_rest = [&](int64_t t) __attribute__((always_inline)) {
+            proc_sweep(0, c0);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                        for (int s = 0; s < R; ++s)
+            for (int xb = 1; xb < SW; xb += B) {
+                Chunks c[B];
 #pragma unroll
-                            for (int u = s + 1; u < R; ++u) {
-                                const uint32_t x = (v[b][s][0] ^ v[b][u][0]) | (v[b][s][1] ^ v[b][u][1]) |
-                                                   (v[b][s][2] ^ v[b][u][2]) | (v[b][s][3] ^ v[b][u][3]);
-                                diff |= (x != 0u ? 1u : 0u) << p;
-                                ++p;
-                            }
-                        if (diff) atomicOr(&pd[i], diff);
-                        const int s_sel = ps[i] & 7;
+                for (int b = 0; b < B; ++b)
+                    if (xb + b < SW) c[b] = load_sweep(t, xb + b);
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            uint32_t w = v[b][0][e];
-#pragma unroll
-                            for (int s = 1; s < R; ++s) w = (s_sel == s) ? v[b][s][e] : w;
-                            keys[xb + b][e] = to_key(w);
-                        }
-                    }
-                }
+                for (int b = 0; b < B; ++b)
+                    if (xb + b < SW) proc_sweep(xb + b, c[b]);
                 // keep each burst's loads together: no scheduling across
                 // bursts, which would hold more loads in registers than fit
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
-        auto put_tile = [&]() {
+        auto put_tile = [&]() __attribute__((always_inline)) {
 #pragma unroll
             for (int x = 0; x < SW; ++x) {
-                const int64_t i = j0 + (int64_t)x * RPI;
+                const int i = j0 + x * RPI;
                 if (i < f) {
                     const int q = ps[i];
                     if (q >= 0) put_keys<T, G>(tile, q >> 3, cq, keys[x]);
                 }
             }
         };
+        // sweep 0 of the next tile is issued before the barrier
+        // and the hand-over, so that loads stay in flight meanwhile
         int64_t t = blockIdx.x;
         if (t < ntiles) {
-            stream_tile(t);
-            put_tile();
+            c0 = load_sweep(t, 0);
+            stream_rest(t);
         }
+        if (t + gridDim.x < ntiles) c0 = load_sweep(t + gridDim.x, 0);
+        if (t < ntiles) put_tile();
         __syncthreads();
         for (; t < ntiles; t += gridDim.x) {
             const int64_t tn = t + gridDim.x;
-            if (tn < ntiles) stream_tile(tn);
+            if (tn < ntiles) stream_rest(tn);
+            if (tn + gridDim.x < ntiles) c0 = load_sweep(tn + gridDim.x, 0);
             __syncthreads();
             if (tn < ntiles) put_tile();
             __syncthreads();
@@ -967,7 +987,7 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
 
 // Warp-specialised single pass: widest tile (>= 8 columns) whose key block
 // and pair-difference words fit in LDS and whose rows fit the streaming
-// role's register budget (at most 20 sweeps of 512 threads).
+// role's register budget (at most 16 sweeps of 512 threads).
 struct WsPlan {
     int T = 0;
     int sweeps = 0;
@@ -980,9 +1000,9 @@ WsPlan ws_plan(int64_t f, int r, bool vec) {
         if (f * 4 * (int64_t)T + f * 8 + hist_words(T) * 4 > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
-        if (sw > 20) continue;
+        if (sw > 16) continue;
         p.T = T;
-        p.sweeps = sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : sw <= 16 ? 16 : 20;
+        p.sweeps = sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         return p;
     }
     return p;
@@ -1011,7 +1031,6 @@ hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Works
     case 8: ASPIS_WS(TT, 8) break;                 \
     case 12: ASPIS_WS(TT, 12) break;               \
     case 16: ASPIS_WS(TT, 16) break;               \
-    case 20: ASPIS_WS(TT, 20) break;               \
     default: return hipErrorInvalidValue;          \
     }
         switch (T) {
