@@ -94,6 +94,35 @@ def copy_probe(torch, aspis, dev, nbytes: int = 1 << 32) -> int:
     return 0
 
 
+def simulate_tables() -> int:
+    """Host-only: aspis_simulate / aspis_detox over the settings of the
+    paper's Section 5 (Tables 1-3, the K=50 sweep of Figure 3) and the
+    K=100, r=5 graphs of the clique-timing tables; prints one JSON line."""
+    from paper_2108_02416_amd import aspis
+    aspis.lib()   # load before timing
+
+    def row(K, r, q, attack):
+        t0 = time.perf_counter()
+        res = aspis.simulate(K, r, q, attack)
+        wall = (time.perf_counter() - t0) * 1e3
+        det = aspis.detox(K, r, q, attack)[1] if K % r == 0 else None
+        return {"K": K, "r": r, "q": q, "attack": attack, "files": res["files"],
+                "distorted": res["distorted"], "epsilon": round(res["epsilon"], 6),
+                "epsilon_baseline": round(res["epsilon_baseline"], 6),
+                "epsilon_detox": None if det is None else round(det, 6),
+                "success": res["success"], "omega": res["omega"],
+                "n_maximum": res["n_maximum"], "ms_clique": round(res["ms_clique"], 4),
+                "ms_files": round(res["ms_files"], 3), "ms_wall": round(wall, 3)}
+
+    tables = [row(K, 3, q, a) for K, qmax in ((15, 7), (21, 10), (24, 11))
+              for a in ("optimal", "weak") for q in range(2, qmax + 1)]
+    k50 = [row(50, 3, q, a) for a in ("optimal", "weak") for q in range(1, 25)]
+    k100 = [row(100, 5, q, a) for a in ("weak", "optimal") for q in (5, 15, 25, 35, 45)]
+    print(json.dumps({"mode": "simulate", "host_threads": min(16, os.cpu_count() or 1),
+                      "tables_1_3": tables, "k50_r3": k50, "k100_r5": k100}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,10 +133,16 @@ def main() -> int:
     ap.add_argument("--two-pass", action="store_true", help="force the two-pass path")
     ap.add_argument("--cpu-sample", type=int, default=1 << 20,
                     help="coordinates of the oracle's CPU-baseline sample (0 = skip)")
+    ap.add_argument("--simulate", action="store_true",
+                    help="instead of the step, run the host distortion-fraction simulator over "
+                         "the paper's tables (K=15, 21, 24), the K=50 sweep and the K=100, r=5 "
+                         "clique-timing setting")
     ap.add_argument("--copy-probe", action="store_true",
                     help="instead of the step, run a plain copy kernel and the read probe "
                          "over 4 GiB (the reference sizes for HBM counter calibration)")
     args = ap.parse_args()
+    if args.simulate:
+        return simulate_tables()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported",
               file=sys.stderr)

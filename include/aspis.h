@@ -197,6 +197,65 @@ size_t aspis_read_probe_sink_words(void);
 aspis_status aspis_read_probe(const void *buf, size_t nbytes, uint32_t *sink,
                               void *stream);
 
+/* ---- distortion-fraction simulator (Section 5, appendix Tables 1-3) ----
+ *
+ * The detect-and-aggregate step on symbolic replicas: every replica is either
+ * its file's true value or the single value all adversaries agree on.  The
+ * simulator runs the same steps as the device path -- pairwise agreement
+ * (Eq. 4), disagreement rows (Eq. 5), vote (Eq. 3), aspis_clique
+ * (Algorithm 3), selection (Algorithm 1) -- over all f = C(K,r) files of
+ * Algorithm 2 and counts the distorted ones.  Host only, synchronous;
+ * multithreaded over file ranks. */
+typedef enum {
+    ASPIS_ATTACK_WEAK = 0,     /* Section 4.1: every adversary distorts every
+                                  file it holds */
+    ASPIS_ATTACK_OPTIMAL = 1   /* Section 4.2, Theorem 1: all adversaries
+                                  disagree with one set D of q honest
+                                  workers: an adversary distorts file F iff
+                                  |F & A| >= (r+1)/2 and F \ A is inside D */
+} aspis_attack;
+
+typedef struct {
+    int64_t files;             /* f = C(K,r)                                 */
+    int64_t distorted;         /* c^(q): files dropped (Case 1, no replica
+                                  from H) or whose selected value is the
+                                  adversaries'                               */
+    int64_t dropped;           /* of which dropped                           */
+    int32_t success;           /* Algorithm 3 detection succeeded (Case 1)   */
+    int32_t omega;             /* size of a maximum clique                   */
+    int32_t n_maximum;         /* number of maximum cliques                  */
+    int32_t reserved;
+    int64_t n_maximal;         /* maximal cliques enumerated                 */
+    double epsilon;            /* distortion fraction distorted / files      */
+    double epsilon_baseline;   /* q / K: aggregation of the K gradients
+                                  without redundancy (Section 5)             */
+    double ms_files;           /* host time of the passes over the files     */
+    double ms_clique;          /* host time of aspis_clique                  */
+} aspis_sim_result;
+
+/* Simulate one attack.
+ *   adversaries    q distinct worker ids, or NULL for {0,..,q-1}
+ *   disagree_set   optimal attack only: q distinct honest worker ids, or
+ *                  NULL for the q lowest-indexed honest workers
+ *   disagree_rows  optional host output, K rows of (K+63)/64 uint64: the
+ *                  disagreement matrix of the simulated round
+ * Requires 3 <= K <= 128, odd 3 <= r <= min(K,15), 0 <= q < K/2 and
+ * C(K,r) <= 2^31.  Errors: INVALID_ARG, OVERFLOW. */
+aspis_status aspis_simulate(int32_t K, int32_t r, int32_t q, aspis_attack attack,
+                            const int32_t *adversaries,
+                            const int32_t *disagree_set, aspis_sim_result *res,
+                            uint64_t *disagree_rows);
+
+/* DETOX, the group-majority scheme Section 5 compares against: K/r groups of
+ * r workers (worker u in group u / r), each group's value decided by
+ * majority.  Adversaries are placed as in Section 5: WEAK puts the i-th
+ * adversary in group i mod (K/r); OPTIMAL (the worst case) fills groups with
+ * (r+1)/2 adversaries each.  Writes the number of groups with an adversarial
+ * majority and epsilon = groups * r / K.  Requires odd r dividing K,
+ * 0 <= q <= K. */
+aspis_status aspis_detox(int32_t K, int32_t r, int32_t q, aspis_attack attack,
+                         int64_t *distorted_groups, double *epsilon);
+
 /* Message describing the calling thread's last failure ("" if none). */
 const char *aspis_last_error(void);
 

@@ -19,13 +19,15 @@ LIB_PATH = os.path.join(HERE, "libaspis.so")
 
 OK, ERR_INVALID_ARG, ERR_OVERFLOW, ERR_BUFFER_SMALL, ERR_DEVICE, ERR_NO_FILES = range(6)
 REDUCE = {"median": 0, "mean": 1, "paper": 2}
+ATTACK = {"weak": 0, "optimal": 1}
 FLAG_TWO_PASS = 1
 FLAG_TIMING = 2
 
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
     "aspis_aggregate_workspace", "aspis_aggregate", "aspis_detect_aggregate",
-    "aspis_read_probe_sink_words", "aspis_read_probe", "aspis_last_error",
+    "aspis_read_probe_sink_words", "aspis_read_probe", "aspis_simulate", "aspis_detox",
+    "aspis_last_error",
 )
 
 
@@ -54,6 +56,20 @@ class CliqueResult(ctypes.Structure):
                 "honest": members(self.honest) if self.success else frozenset(),
                 "detected": members(self.detected) if self.success else frozenset(),
                 "first": members(self.first)}
+
+
+class SimResult(ctypes.Structure):
+    _fields_ = [("files", ctypes.c_int64), ("distorted", ctypes.c_int64),
+                ("dropped", ctypes.c_int64), ("success", ctypes.c_int32),
+                ("omega", ctypes.c_int32), ("n_maximum", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("n_maximal", ctypes.c_int64),
+                ("epsilon", ctypes.c_double), ("epsilon_baseline", ctypes.c_double),
+                ("ms_files", ctypes.c_double), ("ms_clique", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d["success"] = bool(d["success"])
+        return d
 
 
 class RunStats(ctypes.Structure):
@@ -105,6 +121,11 @@ def lib():
     L.aspis_read_probe_sink_words.restype = ctypes.c_size_t
     L.aspis_read_probe.argtypes = [P, ctypes.c_size_t, P, P]
     L.aspis_read_probe.restype = ctypes.c_int
+    L.aspis_simulate.argtypes = [i32, i32, i32, ctypes.c_int, P, P, ctypes.POINTER(SimResult), P]
+    L.aspis_simulate.restype = ctypes.c_int
+    L.aspis_detox.argtypes = [i32, i32, i32, ctypes.c_int, ctypes.POINTER(i64),
+                              ctypes.POINTER(ctypes.c_double)]
+    L.aspis_detox.restype = ctypes.c_int
     L.aspis_last_error.argtypes = []
     L.aspis_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -136,6 +157,38 @@ def clique(disagree_rows: np.ndarray, K: int, q: int) -> CliqueResult:
     res = CliqueResult()
     _check(lib().aspis_clique(rows.ctypes.data, K, q, ctypes.byref(res)))
     return res
+
+
+def simulate(K: int, r: int, q: int, attack: str = "optimal", adversaries=None,
+             disagree_set=None, want_rows: bool = False) -> dict:
+    """Distortion-fraction simulation of one attack on symbolic replicas
+    (aspis_simulate); returns the result fields, plus the disagreement rows
+    when want_rows."""
+    def ids(x):
+        if x is None:
+            return None, None
+        a = np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
+        if a.size != q:
+            raise AspisError(ERR_INVALID_ARG, f"need {q} worker ids, got {a.size}")
+        return a, a.ctypes.data
+    a_arr, a_ptr = ids(adversaries)
+    d_arr, d_ptr = ids(disagree_set)
+    res = SimResult()
+    rows = np.zeros((K, (K + 63) // 64), dtype=np.uint64) if want_rows else None
+    _check(lib().aspis_simulate(K, r, q, ATTACK[attack], a_ptr, d_ptr, ctypes.byref(res),
+                                rows.ctypes.data if rows is not None else None))
+    out = res.as_dict()
+    if want_rows:
+        out["disagree_rows"] = rows
+    return out
+
+
+def detox(K: int, r: int, q: int, attack: str = "optimal") -> tuple[int, float]:
+    """DETOX group-majority distortion (aspis_detox): (groups, epsilon)."""
+    groups = ctypes.c_int64(0)
+    eps = ctypes.c_double(0.0)
+    _check(lib().aspis_detox(K, r, q, ATTACK[attack], ctypes.byref(groups), ctypes.byref(eps)))
+    return int(groups.value), float(eps.value)
 
 
 # -------------------------------------------------------------- device steps

@@ -1,7 +1,8 @@
 """Build libaspis.so (gfx950) in-tree with hipcc.
 
 The library is the C ABI declared in include/aspis.h: host code
-(csrc/aspis_host.cpp) plus the HIP kernels (csrc/aspis_kernels.hip).
+(csrc/aspis_host.cpp, csrc/aspis_sim.cpp) plus the HIP kernels
+(csrc/aspis_kernels.hip).
 """
 import os
 import subprocess
@@ -21,6 +22,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 def build(verbose: bool = False) -> str:
     srcs = [os.path.join(HERE, "csrc", "aspis_host.cpp"),
+            os.path.join(HERE, "csrc", "aspis_sim.cpp"),
             os.path.join(HERE, "csrc", "aspis_kernels.hip")]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -168,6 +168,12 @@ aspis_status check_detect_out(const aspis_detect_out *o) {
 
 }  // namespace
 
+namespace aspis {
+// error reporting for the other host sources of the library
+aspis_status host_fail(aspis_status st, const char *msg) { return fail(st, "%s", msg); }
+void host_clear_error() { g_err[0] = 0; }
+}  // namespace aspis
+
 extern "C" {
 
 const char *aspis_last_error(void) { return g_err; }
