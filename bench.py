@@ -131,6 +131,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--seed", type=int, default=428)
     ap.add_argument("--two-pass", action="store_true", help="force the two-pass path")
+    ap.add_argument("--layout", choices=["file", "worker"], default="file",
+                    help="replicas as one [f][r][d] tensor (file) or as the workers' uploads "
+                         "[K][l][d] (worker, aspis_detect_aggregate_wm)")
     ap.add_argument("--cpu-sample", type=int, default=1 << 20,
                     help="coordinates of the oracle's CPU-baseline sample (0 = skip)")
     ap.add_argument("--simulate", action="store_true",
@@ -167,6 +170,15 @@ def main() -> int:
     t_gen = time.perf_counter()
     grads = torch.empty((f, r, d), dtype=torch.float32, device=dev)
     synth.fill_device(role, worker, grads, wl.dist, seed=args.seed, alie_z=wl.alie_z)
+    if args.layout == "worker":
+        # the same replicas in the order the workers upload them
+        l_files = f * r // K
+        rows = torch.from_numpy(aspis.worker_rows(K, r).reshape(-1).astype(np.int64)).to(dev)
+        upload = torch.empty((K * l_files, d), dtype=torch.float32, device=dev)
+        upload.index_copy_(0, rows, grads.view(f * r, d))
+        del grads, rows
+        torch.cuda.empty_cache()
+        grads = upload.view(K, l_files, d)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
     print(f"# workload {wl.name}: f={f} replicas {wl.replica_bytes() / 1e9:.2f} GB, "
@@ -180,7 +192,7 @@ def main() -> int:
 
     def step():
         return aspis.detect_aggregate(grads, K, r, q, mode="median", flags=flags, bufs=bufs,
-                                      out=out, sel_out=sel, ws=ws)
+                                      out=out, sel_out=sel, ws=ws, layout=args.layout)
 
     for _ in range(args.warmup):
         step()
@@ -224,6 +236,7 @@ def main() -> int:
         "data": "synthetic (seeded Philox, Irwin-Hall N(0,0.01^2) honest gradients, "
                 "ALIE colluders, written on the GPU)",
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
+                   "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
                    "replica_bytes": replica_bytes, "parallelism": "single GPU"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),

@@ -129,9 +129,10 @@ typedef struct {
 aspis_status aspis_clique(const uint64_t *disagree_rows, int32_t K, int32_t q,
                           aspis_clique_result *res);
 
-/* Bytes of workspace aspis_aggregate and aspis_detect_aggregate need: four
- * int32 [f] arrays, each rounded up to 256 bytes, plus 256 bytes of
- * counters.  0 on invalid arguments. */
+/* Bytes of workspace aspis_aggregate, aspis_detect_aggregate and
+ * aspis_detect_aggregate_wm need: four int32 [f] arrays and one int32
+ * [f*r] table, each rounded up to 256 bytes, plus 256 bytes of counters.
+ * 0 on invalid arguments. */
 size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d);
 
 /* Algorithm 1, aggregation.  Selection: on success (Case 1) file i keeps
@@ -189,6 +190,32 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
                                     int64_t *n_selected, void *workspace,
                                     size_t ws_bytes, uint32_t flags,
                                     aspis_run_stats *stats, void *stream);
+
+/* The worker-major upload of Algorithm 1: worker u returns the gradients
+ * of its l = C(K-1,r-1) files in ascending file order, one after another,
+ * so the upload of all K workers is a float32 [K][l][d] tensor.  Writes, for
+ * every replica (i,s), its row in that tensor: row_of[i*r + s] = u*l + k
+ * where u is the worker of slot s of file i and i is u's k-th file (host
+ * memory, caller-owned, at least cap_entries = f*r entries).
+ * Errors: INVALID_ARG, OVERFLOW, BUFFER_SMALL (nothing written). */
+aspis_status aspis_worker_rows(int32_t K, int32_t r, int32_t *row_of,
+                               int64_t cap_entries);
+
+/* aspis_detect_aggregate on the worker-major upload grads_wm (float32
+ * [K][l][d], contiguous, device) instead of the file-major [f][r][d]
+ * tensor: the same steps, outputs and errors, the rows read through the
+ * table of aspis_worker_rows (which the library builds in the workspace).
+ * The pair-difference words, votes, selection (slot per file) and result
+ * are identical to aspis_detect_aggregate's on the same replicas. */
+aspis_status aspis_detect_aggregate_wm(const float *grads_wm, int32_t K, int32_t r,
+                                       int32_t q, int64_t d,
+                                       const int32_t *subsets_dev,
+                                       const aspis_detect_out *det,
+                                       aspis_reduce mode, float *out,
+                                       int32_t *sel_out, aspis_clique_result *res,
+                                       int64_t *n_selected, void *workspace,
+                                       size_t ws_bytes, uint32_t flags,
+                                       aspis_run_stats *stats, void *stream);
 
 /* Diagnostic: streams nbytes (multiple of 16) of device memory and writes a
  * checksum word per thread to sink (device, >= aspis_read_probe_sink_words()

@@ -26,6 +26,7 @@ FLAG_TIMING = 2
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
     "aspis_aggregate_workspace", "aspis_aggregate", "aspis_detect_aggregate",
+    "aspis_detect_aggregate_wm", "aspis_worker_rows",
     "aspis_read_probe_sink_words", "aspis_read_probe", "aspis_simulate", "aspis_detox",
     "aspis_last_error",
 )
@@ -117,6 +118,10 @@ def lib():
                                          ctypes.POINTER(i64), P, ctypes.c_size_t, u32,
                                          ctypes.POINTER(RunStats), P]
     L.aspis_detect_aggregate.restype = ctypes.c_int
+    L.aspis_detect_aggregate_wm.argtypes = L.aspis_detect_aggregate.argtypes
+    L.aspis_detect_aggregate_wm.restype = ctypes.c_int
+    L.aspis_worker_rows.argtypes = [i32, i32, P, i64]
+    L.aspis_worker_rows.restype = ctypes.c_int
     L.aspis_read_probe_sink_words.argtypes = []
     L.aspis_read_probe_sink_words.restype = ctypes.c_size_t
     L.aspis_read_probe.argtypes = [P, ctypes.c_size_t, P, P]
@@ -149,6 +154,17 @@ def assign(K: int, r: int) -> np.ndarray:
         raise AspisError(ERR_INVALID_ARG, f"invalid (K={K}, r={r})")
     out = np.zeros((f, r), dtype=np.int32)
     _check(lib().aspis_assign(K, r, out.ctypes.data, f))
+    return out
+
+
+def worker_rows(K: int, r: int) -> np.ndarray:
+    """Row of replica (i, s) in the worker-major upload [K][l][d]:
+    int32 [f, r] (aspis_worker_rows)."""
+    f = num_files(K, r)
+    if f <= 0:
+        raise AspisError(ERR_INVALID_ARG, f"invalid (K={K}, r={r})")
+    out = np.zeros((f, r), dtype=np.int32)
+    _check(lib().aspis_worker_rows(K, r, out.ctypes.data, f * r))
     return out
 
 
@@ -286,12 +302,27 @@ def aggregate(grads, K: int, r: int, bufs: DetectBuffers, res: CliqueResult,
     return out, int(n_sel.value)
 
 
+def _check_grads_wm(grads, K: int, r: int):
+    torch = _torch()
+    f = num_files(K, r)
+    l_files = f * r // K
+    if not (grads.is_cuda and grads.dtype == torch.float32 and grads.dim() == 3
+            and grads.is_contiguous() and grads.shape[0] == K and grads.shape[1] == l_files):
+        raise AspisError(ERR_INVALID_ARG,
+                         f"grads must be a contiguous cuda float32 [{K}, {l_files}, d] tensor")
+    return f, grads.shape[2]
+
+
 def detect_aggregate(grads, K: int, r: int, q: int, mode: str = "median", flags: int = 0,
                      bufs: DetectBuffers | None = None, out=None, sel_out=None, ws=None,
-                     want_sel: bool = True) -> dict:
-    """The whole step (Algorithm 3 then Algorithm 1) in one library call."""
+                     want_sel: bool = True, layout: str = "file") -> dict:
+    """The whole step (Algorithm 3 then Algorithm 1) in one library call.
+    layout "file": grads is [f][r][d]; "worker": grads is the workers'
+    upload [K][l][d] (aspis_detect_aggregate_wm)."""
     torch = _torch()
-    f, d = _check_grads(grads, K, r)
+    if layout not in ("file", "worker"):
+        raise AspisError(ERR_INVALID_ARG, f"unknown layout {layout!r}")
+    f, d = (_check_grads if layout == "file" else _check_grads_wm)(grads, K, r)
     bufs = bufs or DetectBuffers.empty(f, K, grads.device)
     out = out if out is not None else torch.empty(d, dtype=torch.float32, device=grads.device)
     if sel_out is None and want_sel:
@@ -302,7 +333,8 @@ def detect_aggregate(grads, K: int, r: int, q: int, mode: str = "median", flags:
     stats = RunStats()
     n_sel = ctypes.c_int64(0)
     det = bufs.c()
-    st = lib().aspis_detect_aggregate(
+    entry = lib().aspis_detect_aggregate if layout == "file" else lib().aspis_detect_aggregate_wm
+    st = entry(
         grads.data_ptr(), K, r, q, d, subsets_device(K, r, grads.device).data_ptr(),
         ctypes.byref(det), REDUCE[mode], out.data_ptr(),
         sel_out.data_ptr() if sel_out is not None else None, ctypes.byref(res),

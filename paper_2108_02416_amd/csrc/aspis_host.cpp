@@ -250,11 +250,32 @@ aspis_status aspis_clique(const uint64_t *rows, int32_t K, int32_t q, aspis_cliq
 size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d) {
     int64_t f = 0;
     if (check_device_shape(K, r, d, &f) != ASPIS_OK) return 0;
-    return aspis::workspace_bytes(f);
+    return aspis::workspace_bytes(f, r);
 }
 
-aspis_status aspis_detect(const float *grads, int32_t K, int32_t r, int64_t d,
-                          const int32_t *subsets_dev, const aspis_detect_out *out, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The worker-major upload of Algorithm 1: worker u returns the gradients of
+// its l = C(K-1,r-1) files in ascending file order, so replica (i,s) is row
+// u*l + k of the upload, where u is slot s's worker and file i is the k-th
+// file of u.
+void worker_row_table(int32_t K, int32_t r, int32_t *row_of) {
+    const int64_t f = binom(K, r), l = binom(K - 1, r - 1);
+    std::vector<int32_t> subsets((size_t)f * r), cur(r), next_local(K, 0);
+    int32_t *dst = subsets.data();
+    emit_subsets(K, r, 0, 0, cur.data(), dst);
+    for (int64_t i = 0; i < f; ++i)
+        for (int s = 0; s < r; ++s) {
+            const int32_t u = subsets[(size_t)i * r + s];
+            row_of[(size_t)i * r + s] = (int32_t)(u * l + next_local[u]++);
+        }
+}
+
+aspis_status detect_impl(const float *grads, const int32_t *row_of, int32_t K, int32_t r,
+                         int64_t d, const int32_t *subsets_dev, const aspis_detect_out *out,
+                         void *stream) {
     int64_t f = 0;
     aspis_status st = check_device_shape(K, r, d, &f);
     if (st != ASPIS_OK) return st;
@@ -263,17 +284,17 @@ aspis_status aspis_detect(const float *grads, int32_t K, int32_t r, int64_t d,
     hipStream_t s = static_cast<hipStream_t>(stream);
     ASPIS_HIP(aspis::launch_fill_u32(out->pair_diff, f, 0u, s));
     ASPIS_HIP(aspis::launch_fill_u64(out->disagree, K, 0ull, s));
-    ASPIS_HIP(aspis::launch_agree(grads, f, r, d, d, out->pair_diff, s));
+    ASPIS_HIP(aspis::launch_agree(grads, row_of, f, r, d, d, out->pair_diff, s));
     ASPIS_HIP(aspis::launch_vote(out->pair_diff, subsets_dev, f, r, out->vote, out->has_majority,
                                  out->disagree, s));
     return ASPIS_OK;
 }
 
-aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d,
-                             const int32_t *subsets_dev, const aspis_detect_out *det,
-                             const aspis_clique_result *res, aspis_reduce mode, float *out,
-                             int32_t *sel_out, int64_t *n_selected, void *workspace,
-                             size_t ws_bytes, void *stream) {
+aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K, int32_t r,
+                            int64_t d, const int32_t *subsets_dev, const aspis_detect_out *det,
+                            const aspis_clique_result *res, aspis_reduce mode, float *out,
+                            int32_t *sel_out, int64_t *n_selected, void *workspace,
+                            size_t ws_bytes, void *stream) {
     int64_t f = 0;
     aspis_status st = check_device_shape(K, r, d, &f);
     if (st != ASPIS_OK) return st;
@@ -281,8 +302,8 @@ aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d
         return fail(ASPIS_ERR_INVALID_ARG, "aspis_aggregate: NULL argument");
     if (mode != ASPIS_REDUCE_MEDIAN && mode != ASPIS_REDUCE_MEAN && mode != ASPIS_REDUCE_PAPER)
         return fail(ASPIS_ERR_INVALID_ARG, "aspis_aggregate: unknown mode %d", (int)mode);
-    if (ws_bytes < aspis::workspace_bytes(f))
-        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f));
+    if (ws_bytes < aspis::workspace_bytes(f, r))
+        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f, r));
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     if (res->success && (res->honest[1] != 0 || K > 64))
@@ -294,9 +315,9 @@ aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d
         return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
                     (long long)aspis::median_capacity(4));
     hipStream_t s = static_cast<hipStream_t>(stream);
-    aspis::Workspace ws = aspis::carve_workspace(workspace, f);
-    ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success, honest_mask(res), ws,
-                                   false, sel_out, s));
+    aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
+    ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success, honest_mask(res),
+                                   row_of, ws, false, sel_out, s));
     if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
     if (mean)
         ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
@@ -305,12 +326,12 @@ aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d
     return ASPIS_OK;
 }
 
-aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, int32_t q, int64_t d,
-                                    const int32_t *subsets_dev, const aspis_detect_out *det,
-                                    aspis_reduce mode, float *out, int32_t *sel_out,
-                                    aspis_clique_result *res, int64_t *n_selected, void *workspace,
-                                    size_t ws_bytes, uint32_t flags, aspis_run_stats *stats,
-                                    void *stream) {
+aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_t K, int32_t r,
+                                   int32_t q, int64_t d, const int32_t *subsets_dev,
+                                   const aspis_detect_out *det, aspis_reduce mode, float *out,
+                                   int32_t *sel_out, aspis_clique_result *res,
+                                   int64_t *n_selected, void *workspace, size_t ws_bytes,
+                                   uint32_t flags, aspis_run_stats *stats, void *stream) {
     using clk = std::chrono::steady_clock;
     const auto t0 = clk::now();
     int64_t f = 0;
@@ -322,8 +343,8 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
     if (q < 0 || 2 * q >= K) return fail(ASPIS_ERR_INVALID_ARG, "q=%d outside [0,K/2)", q);
     if (mode != ASPIS_REDUCE_MEDIAN && mode != ASPIS_REDUCE_MEAN && mode != ASPIS_REDUCE_PAPER)
         return fail(ASPIS_ERR_INVALID_ARG, "unknown mode %d", (int)mode);
-    if (ws_bytes < aspis::workspace_bytes(f))
-        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f));
+    if (ws_bytes < aspis::workspace_bytes(f, r))
+        return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f, r));
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     if (mode != ASPIS_REDUCE_MEAN && aspis::pick_median_tile(f) == 0)
@@ -347,7 +368,18 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
         ASPIS_HIP(hipStreamSynchronize(s));
         return aspis_clique(rows.data(), K, q, out_res);
     };
-    aspis::Workspace ws = aspis::carve_workspace(workspace, f);
+    aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
+    // the row of every replica in a worker-major upload, in the workspace
+    // (kept alive until the stream has been synchronised below)
+    std::vector<int32_t> host_rows;
+    const int32_t *row_of = nullptr;
+    if (worker_major) {
+        host_rows.resize((size_t)f * r);
+        worker_row_table(K, r, host_rows.data());
+        ASPIS_HIP(hipMemcpyAsync(ws.row_of, host_rows.data(), host_rows.size() * sizeof(int32_t),
+                                 hipMemcpyHostToDevice, s));
+        row_of = ws.row_of;
+    }
 
     const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) && mode != ASPIS_REDUCE_MEAN &&
                            aspis::fused_supported(f, r);
@@ -358,7 +390,7 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
         if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
         ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
         ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
-        ASPIS_HIP(aspis::launch_agree(grads, f, r, d, probe, det->pair_diff, s));
+        ASPIS_HIP(aspis::launch_agree(grads, row_of, f, r, d, probe, det->pair_diff, s));
         ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote, det->has_majority,
                                      det->disagree, s));
         if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
@@ -367,11 +399,11 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
         if (!use_mean(mode, &guess)) {
             local.fused = 1;
             ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, guess.success,
-                                           honest_mask(&guess), ws, false, nullptr, s));
+                                           honest_mask(&guess), row_of, ws, false, nullptr, s));
             // 2) one pass: agreement on every coordinate + median with the guess
             ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
-            ASPIS_HIP(aspis::launch_fused(grads, f, r, d, ws, det->pair_diff, out, s));
+            ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
             ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
             ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote,
@@ -383,7 +415,7 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
             if (n_selected) *n_selected = m;
             ASPIS_HIP(aspis::launch_fill_u32(reinterpret_cast<uint32_t *>(ws.flag), 1, 0u, s));
             ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
-                                           honest_mask(res), ws, true, sel_out, s));
+                                           honest_mask(res), row_of, ws, true, sel_out, s));
             ASPIS_HIP(aspis::launch_compare_sel(ws.sel, ws.sel2, f, ws.flag, s));
             int32_t flag = 0;
             ASPIS_HIP(hipMemcpyAsync(&flag, ws.flag, sizeof flag, hipMemcpyDeviceToHost, s));
@@ -414,10 +446,13 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
     }
     // two-pass: full agreement, clique, then selection and reduction
     if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
-    if ((st = aspis_detect(grads, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) { destroy(); return st; }
+    if ((st = detect_impl(grads, row_of, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) {
+        destroy();
+        return st;
+    }
     if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
-    st = aspis_aggregate(grads, K, r, d, subsets_dev, det, res, mode, out, sel_out, n_selected,
-                         workspace, ws_bytes, stream);
+    st = aggregate_impl(grads, row_of, K, r, d, subsets_dev, det, res, mode, out, sel_out,
+                        n_selected, workspace, ws_bytes, stream);
     if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
     ASPIS_HIP(hipStreamSynchronize(s));
     if (timing) ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));
@@ -425,6 +460,57 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
     local.ms_total = std::chrono::duration<float, std::milli>(clk::now() - t0).count();
     if (stats) *stats = local;
     return st;
+}
+
+
+}  // namespace
+
+extern "C" {
+
+aspis_status aspis_detect(const float *grads, int32_t K, int32_t r, int64_t d,
+                          const int32_t *subsets_dev, const aspis_detect_out *out, void *stream) {
+    return detect_impl(grads, nullptr, K, r, d, subsets_dev, out, stream);
+}
+
+aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r, int64_t d,
+                             const int32_t *subsets_dev, const aspis_detect_out *det,
+                             const aspis_clique_result *res, aspis_reduce mode, float *out,
+                             int32_t *sel_out, int64_t *n_selected, void *workspace,
+                             size_t ws_bytes, void *stream) {
+    return aggregate_impl(grads, nullptr, K, r, d, subsets_dev, det, res, mode, out, sel_out,
+                          n_selected, workspace, ws_bytes, stream);
+}
+
+aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, int32_t q, int64_t d,
+                                    const int32_t *subsets_dev, const aspis_detect_out *det,
+                                    aspis_reduce mode, float *out, int32_t *sel_out,
+                                    aspis_clique_result *res, int64_t *n_selected, void *workspace,
+                                    size_t ws_bytes, uint32_t flags, aspis_run_stats *stats,
+                                    void *stream) {
+    return detect_aggregate_impl(grads, false, K, r, q, d, subsets_dev, det, mode, out, sel_out,
+                                 res, n_selected, workspace, ws_bytes, flags, stats, stream);
+}
+
+aspis_status aspis_detect_aggregate_wm(const float *grads_wm, int32_t K, int32_t r, int32_t q,
+                                       int64_t d, const int32_t *subsets_dev,
+                                       const aspis_detect_out *det, aspis_reduce mode, float *out,
+                                       int32_t *sel_out, aspis_clique_result *res,
+                                       int64_t *n_selected, void *workspace, size_t ws_bytes,
+                                       uint32_t flags, aspis_run_stats *stats, void *stream) {
+    return detect_aggregate_impl(grads_wm, true, K, r, q, d, subsets_dev, det, mode, out, sel_out,
+                                 res, n_selected, workspace, ws_bytes, flags, stats, stream);
+}
+
+aspis_status aspis_worker_rows(int32_t K, int32_t r, int32_t *row_of, int64_t cap_entries) {
+    if (K < 1 || r < 1 || r > K || row_of == nullptr)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_worker_rows: need 1 <= r <= K and a buffer");
+    const int64_t f = binom(K, r);
+    if (f < 0 || f > INT32_MAX / r) return fail(ASPIS_ERR_OVERFLOW, "C(%d,%d)*r overflows int32", K, r);
+    if (f * r > cap_entries)
+        return fail(ASPIS_ERR_BUFFER_SMALL, "need %lld entries, buffer holds %lld",
+                    (long long)(f * r), (long long)cap_entries);
+    worker_row_table(K, r, row_of);
+    return ASPIS_OK;
 }
 
 size_t aspis_read_probe_sink_words(void) { return aspis::read_probe_sink_words(); }

@@ -30,16 +30,20 @@ struct Workspace {
     int32_t *rows;   // [f] kept replica rows (i*r + slot), file order
     int32_t *n_sel;  // [1] number of kept files
     int32_t *flag;   // [1] scratch flag
+    int32_t *row_of; // [f*r] row of replica (i,s) in a worker-major upload
 };
-size_t workspace_bytes(int64_t f);
-Workspace carve_workspace(void *base, int64_t f);
+size_t workspace_bytes(int64_t f, int r);
+Workspace carve_workspace(void *base, int64_t f, int r);
 
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
 
+// Replica (i,s) is row i*r+s of g (file-major, row_of == nullptr) or row
+// row_of[i*r+s] (a device table, e.g. the worker-major upload order).
+
 // Pairwise agreement over coordinates [0, k_end) of every file; ORs the
 // per-file pair-difference bits into pair_diff (which the caller zeroes).
-hipError_t launch_agree(const float *g, int64_t f, int r, int64_t d,
+hipError_t launch_agree(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         int64_t k_end, uint32_t *pair_diff, hipStream_t s);
 
 // Per-file vote / majority flag and the disagreement rows (caller zeroes
@@ -51,10 +55,11 @@ hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets,
 // Selection of Algorithm 1 into the workspace (sel, pos, rows, n_sel).
 // sel is written to ws.sel, or to ws.sel2 when into_sel2 is set, and also
 // to sel_out when it is not NULL.
+// ws.rows lists the kept rows of g (through row_of when it is not NULL).
 hipError_t launch_select(const int32_t *subsets, const int8_t *vote,
                          int64_t f, int r, int success, uint64_t honest,
-                         const Workspace &ws, bool into_sel2, int32_t *sel_out,
-                         hipStream_t s);
+                         const int32_t *row_of, const Workspace &ws, bool into_sel2,
+                         int32_t *sel_out, hipStream_t s);
 
 // Tile width the median kernel uses for up to f kept files (0: too many).
 int pick_median_tile(int64_t f);
@@ -67,7 +72,7 @@ hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
 
 // Single pass: agreement bits of every file over [0, d) and the median of
 // the rows selected by ws (a guess), in one read of the replica tensor.
-hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d,
+hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         const Workspace &ws, uint32_t *pair_diff, float *out,
                         hipStream_t s);
 bool fused_supported(int64_t f, int r);

@@ -372,15 +372,23 @@ __global__ void fill_u64_kernel(uint64_t *p, int64_t n, uint64_t v) {
 constexpr int kAgreeUnroll = 4;                       // float4 per thread
 constexpr int64_t kAgreeChunk = (int64_t)kBlock * 4 * kAgreeUnroll;
 
+// Row of replica (i,s): i*R+s in the file-major tensor, or row_of[i*R+s]
+// when a row table is given.
+__device__ __forceinline__ int64_t replica_row(const int32_t *row_of, int64_t i, int R, int s) {
+    return row_of ? (int64_t)row_of[i * R + s] : i * R + s;
+}
+
 template <int R, bool VEC>
 __global__ void __launch_bounds__(kBlock)
-agree_kernel(const float *__restrict__ g, int64_t f, int64_t d, int64_t kend,
-             int64_t nchunks, uint32_t *__restrict__ pair_diff) {
+agree_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
+             int64_t d, int64_t kend, int64_t nchunks, uint32_t *__restrict__ pair_diff) {
     const int64_t nwork = f * nchunks;
     for (int64_t w = blockIdx.x; w < nwork; w += gridDim.x) {
         const int64_t i = w / nchunks;
         const int64_t chunk = w - i * nchunks;
-        const float *rows = g + i * R * d;
+        const float *rows[R];
+#pragma unroll
+        for (int s = 0; s < R; ++s) rows[s] = g + replica_row(row_of, i, R, s) * d;
         uint32_t diff = 0u;
 #pragma unroll
         for (int u = 0; u < kAgreeUnroll; ++u) {
@@ -389,7 +397,7 @@ agree_kernel(const float *__restrict__ g, int64_t f, int64_t d, int64_t kend,
             if (k < kend) {
                 uint32_t v[R][4];
 #pragma unroll
-                for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k, kend, v[s]);
+                for (int s = 0; s < R; ++s) load4<VEC>(rows[s], k, kend, v[s]);
                 int p = 0;
 #pragma unroll
                 for (int s = 0; s < R; ++s)
@@ -457,8 +465,8 @@ __global__ void vote_kernel(const uint32_t *__restrict__ pair_diff,
 __global__ void __launch_bounds__(1024)
 select_kernel(const int32_t *__restrict__ subsets,
               const int8_t *__restrict__ vote, int64_t f, int r,
-              int success, uint64_t honest, int32_t *__restrict__ sel,
-              int32_t *__restrict__ pos, int32_t *__restrict__ rows,
+              int success, uint64_t honest, const int32_t *__restrict__ row_of,
+              int32_t *__restrict__ sel, int32_t *__restrict__ pos, int32_t *__restrict__ rows,
               int32_t *__restrict__ n_sel, int32_t *__restrict__ sel_out) {
     __shared__ int wave_tot[16];
     __shared__ int carry;
@@ -491,7 +499,7 @@ select_kernel(const int32_t *__restrict__ subsets,
             sel[i] = s;
             pos[i] = p;
             if (sel_out) sel_out[i] = s;
-            if (keep) rows[p] = (int32_t)(i * r + s);
+            if (keep) rows[p] = row_of ? row_of[i * r + s] : (int32_t)(i * r + s);
         }
         __syncthreads();
         if (tid == 0) {
@@ -567,7 +575,7 @@ constexpr int fused_batch() { return R == 3 ? 4 : (R == 5 ? 2 : 1); }
 
 template <int T, int R, bool VEC>
 __global__ void __launch_bounds__(tile_block<T>())
-fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
+fused_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
              const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
              const int32_t *__restrict__ n_sel, int64_t ntiles,
              uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
@@ -594,9 +602,9 @@ fused_kernel(const float *__restrict__ g, int64_t f, int64_t d,
             for (int b = 0; b < B; ++b) {
                 const int64_t i = ib + b * RPI + j0;
                 if (i < f) {
-                    const float *rows = g + i * R * d;
 #pragma unroll
-                    for (int s = 0; s < R; ++s) load4<VEC>(rows + s * d, k0 + 4 * cq, d, v[b][s]);
+                    for (int s = 0; s < R; ++s)
+                        load4<VEC>(g + replica_row(row_of, i, R, s) * d, k0 + 4 * cq, d, v[b][s]);
                 }
             }
 #pragma unroll
@@ -654,9 +662,9 @@ constexpr int kWsSelect = 512;     // threads of the selection role
 template <int R, int SW>
 constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
 
-template <int T, int R, int SW>
+template <int T, int R, int SW, bool IND>
 __global__ void __launch_bounds__(kWsFill + kWsSelect)
-fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
+fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
                 const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
                 const int32_t *__restrict__ n_sel, int64_t ntiles,
                 uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
@@ -670,11 +678,14 @@ fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
     uint32_t *tile = smem + hist_words(T);
     uint32_t *pd = tile + f * T;         // [f] per-workgroup pair-difference bits
     int32_t *ps = reinterpret_cast<int32_t *>(pd + f);   // [f] (tile row << 3) | slot, or -1
+    int32_t *rt = ps + f;                // [f*R] row table (IND)
     const int tid = threadIdx.x;
     for (int64_t i = tid; i < f; i += kWsFill + kWsSelect) {
         pd[i] = 0u;
         ps[i] = pos[i] >= 0 ? (pos[i] << 3) | sel[i] : -1;
     }
+    if constexpr (IND)
+        for (int64_t i = tid; i < f * R; i += kWsFill + kWsSelect) rt[i] = row_of[i];
     for (int i = tid; i < hist_words(T); i += kWsFill + kWsSelect) hist[i] = 0u;
     __syncthreads();
     // roles are whole waves: waves 0-7 stream, waves 8-15 select; every wave
@@ -697,6 +708,14 @@ fused_ws_kernel(const float *__restrict__ g, int64_t f, int64_t d,
         // any written median.
         auto load_sweep = [&](int64_t t, int x) __attribute__((always_inline)) {
             const int64_t col = min(t * T + 4 * cq, d - 4);
+            if constexpr (IND) {
+                const int i = j0 + x * RPI < f ? j0 + x * RPI : 0;
+                Chunks c;
+#pragma unroll
+                for (int s = 0; s < R; ++s)
+                    c.q[s] = *reinterpret_cast<const uint4 *>(g + (int64_t)rt[i * R + s] * d + col);
+                return c;
+            }
             const float *base = g + (int64_t)j0 * R * d + col;
             int lim = (int)(f - j0);   // sweeps x with x * RPI < lim hold a file
             // opaque copies of the tile's base address and of the limit:
@@ -879,14 +898,14 @@ int64_t tile_grid(int64_t ntiles, size_t lds) {
 // ---------------------------------------------------------------------------
 // launchers
 
-size_t workspace_bytes(int64_t f) {
+size_t workspace_bytes(int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up((size_t)f * 4) * 4 + 256;
+    return up((size_t)f * 4) * 4 + 256 + up((size_t)f * r * 4);
 }
 
 int pick_median_tile(int64_t f) { return pick_tile(f, 0); }
 
-Workspace carve_workspace(void *base, int64_t f) {
+Workspace carve_workspace(void *base, int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
     char *p = static_cast<char *>(base);
     Workspace w;
@@ -900,6 +919,9 @@ Workspace carve_workspace(void *base, int64_t f) {
     p += up((size_t)f * 4);
     w.n_sel = reinterpret_cast<int32_t *>(p);
     w.flag = w.n_sel + 1;
+    p += 256;
+    w.row_of = reinterpret_cast<int32_t *>(p);
+    (void)r;   // the table holds f*r entries (workspace_bytes)
     return w;
 }
 
@@ -914,17 +936,17 @@ hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_agree(const float *g, int64_t f, int r, int64_t d, int64_t kend,
-                        uint32_t *pair_diff, hipStream_t s) {
+hipError_t launch_agree(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                        int64_t kend, uint32_t *pair_diff, hipStream_t s) {
     if (kend <= 0 || f <= 0) return hipSuccess;
     const int64_t nchunks = (kend + kAgreeChunk - 1) / kAgreeChunk;
     const unsigned grid = (unsigned)grid_for(f * nchunks, (int64_t)num_cus() * 16);
     const bool vec = (d % 4 == 0) && aligned16(g);
 #define ASPIS_AGREE(RR)                                                              \
     if (vec)                                                                         \
-        agree_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, f, d, kend, nchunks, pair_diff); \
+        agree_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, nchunks, pair_diff); \
     else                                                                             \
-        agree_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, f, d, kend, nchunks, pair_diff);
+        agree_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, nchunks, pair_diff);
     switch (r) {
     case 3: ASPIS_AGREE(3) break;
     case 5: ASPIS_AGREE(5) break;
@@ -944,9 +966,9 @@ hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets, int64_
 }
 
 hipError_t launch_select(const int32_t *subsets, const int8_t *vote, int64_t f, int r,
-                         int success, uint64_t honest, const Workspace &ws, bool into_sel2,
-                         int32_t *sel_out, hipStream_t s) {
-    select_kernel<<<1, 1024, 0, s>>>(subsets, vote, f, r, success, honest,
+                         int success, uint64_t honest, const int32_t *row_of, const Workspace &ws,
+                         bool into_sel2, int32_t *sel_out, hipStream_t s) {
+    select_kernel<<<1, 1024, 0, s>>>(subsets, vote, f, r, success, honest, row_of,
                                      into_sel2 ? ws.sel2 : ws.sel, ws.pos, ws.rows, ws.n_sel,
                                      sel_out);
     return hipGetLastError();
@@ -993,11 +1015,17 @@ struct WsPlan {
     int sweeps = 0;
 };
 
-WsPlan ws_plan(int64_t f, int r, bool vec) {
+// LDS of the warp-specialised kernel: histograms, key tile, per-file words
+// and, with a row table, the table.
+int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind) {
+    return hist_words(T) * 4 + f * 4 * (int64_t)T + f * 8 + (ind ? f * r * 4 : 0);
+}
+
+WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     WsPlan p;
     if (r != 3 || !vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (f * 4 * (int64_t)T + f * 8 + hist_words(T) * 4 > kLdsBytes) continue;
+        if (ws_lds_bytes(f, r, T, ind) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         if (sw > 16) continue;
@@ -1012,18 +1040,23 @@ bool fused_supported(int64_t f, int r) {
     return (r == 3 || r == 5 || r == 7) && pick_tile(f, f * 4) != 0;
 }
 
-hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Workspace &ws,
-                        uint32_t *pair_diff, float *out, hipStream_t s) {
+hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                        const Workspace &ws, uint32_t *pair_diff, float *out, hipStream_t s) {
     const bool vec = (d % 4 == 0) && aligned16(g);
-    const WsPlan plan = ws_plan(f, r, vec);
+    const bool ind = row_of != nullptr;
+    const WsPlan plan = ws_plan(f, r, vec, ind);
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)(f * 4 * T + f * 8 + hist_words(T) * 4);
+        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
 #define ASPIS_WS(TT, SWW)                                                                        \
-    fused_ws_kernel<TT, 3, SWW><<<grid, kWsFill + kWsSelect, lds, s>>>(                          \
-        g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+    if (ind)                                                                                     \
+        fused_ws_kernel<TT, 3, SWW, true><<<grid, kWsFill + kWsSelect, lds, s>>>(                \
+            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                  \
+    else                                                                                         \
+        fused_ws_kernel<TT, 3, SWW, false><<<grid, kWsFill + kWsSelect, lds, s>>>(               \
+            g, nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_WS_T(TT)                             \
     switch (plan.sweeps) {                         \
     case 2: ASPIS_WS(TT, 2) break;                 \
@@ -1052,10 +1085,10 @@ hipError_t launch_fused(const float *g, int64_t f, int r, int64_t d, const Works
 #define ASPIS_FUSED(TT, RR)                                                                  \
     if (vec)                                                                                 \
         fused_kernel<TT, RR, true><<<grid, tile_block<TT>(), lds, s>>>(                      \
-            g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                      \
+            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);              \
     else                                                                                     \
         fused_kernel<TT, RR, false><<<grid, tile_block<TT>(), lds, s>>>(                     \
-            g, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_FUSED_R(TT)                     \
     switch (r) {                              \
     case 3: ASPIS_FUSED(TT, 3) break;         \

@@ -1,0 +1,103 @@
+"""GPU parity of the worker-major entry point (aspis_detect_aggregate_wm):
+the replicas are laid out as the workers upload them, [K][l][d], built here
+from the oracle's assignment, and every output must equal the oracle's on
+the file-major tensor -- and the file-major GPU path's, bit for bit."""
+from math import comb
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from paper_2108_02416_amd import aspis
+
+from _helpers import assert_detection, assert_same_floats, device, to_np
+from test_worker_rows import expected_rows
+
+pytestmark = pytest.mark.gpu
+
+
+def to_worker_major(g: np.ndarray, K: int, r: int) -> np.ndarray:
+    f, _, d = g.shape
+    l_files = comb(K - 1, r - 1)
+    rows = expected_rows(K, r).reshape(-1)
+    wm = np.empty((K * l_files, d), dtype=np.float32)
+    wm[rows] = g.reshape(f * r, d)
+    return wm.reshape(K, l_files, d)
+
+
+def _run_both(g, K, r, q, mode, flags):
+    import torch
+    dev = device()
+    fm = torch.from_numpy(np.ascontiguousarray(g)).to(dev)
+    wm = torch.from_numpy(to_worker_major(g, K, r)).to(dev)
+    a = aspis.detect_aggregate(fm, K, r, q, mode=mode, flags=flags | aspis.FLAG_TIMING)
+    b = aspis.detect_aggregate(wm, K, r, q, mode=mode, flags=flags | aspis.FLAG_TIMING,
+                               layout="worker")
+    torch.cuda.synchronize()
+    return a, b
+
+
+def _check(g, K, r, q, mode="median", flags=0):
+    ref = oracle.run(g, K, r, q, mode=mode)
+    a, b = _run_both(g, K, r, q, mode, flags)
+    assert_detection(b, ref, K)
+    assert (to_np(b["sel"]) == ref["sel"]).all()
+    assert b["n_selected"] == ref["n_selected"]
+    assert_same_floats(to_np(b["out"]), ref["out"])
+    assert_same_floats(to_np(b["out"]), to_np(a["out"]))
+    assert b["stats"]["fused"] == a["stats"]["fused"]
+    return b, ref
+
+
+_D = {1: 4099, 2: 2056, 3: 1548, 4: 523, 5: 392}
+
+
+@pytest.mark.parametrize("flags", [0, aspis.FLAG_TWO_PASS])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_workloads_worker_major(idx, flags):
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D[idx])
+    _check(g, wl.K, wl.r, wl.q, flags=flags)
+
+
+@pytest.mark.parametrize("mode", ["mean", "paper"])
+def test_modes_worker_major(mode):
+    wl = synth.WORKLOADS[2]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=3001)
+    _check(g, wl.K, wl.r, wl.q, mode=mode)
+
+
+@pytest.mark.parametrize("K,r,d", [(9, 5, 333), (13, 5, 132), (9, 7, 260)])
+def test_wider_files_worker_major(K, r, d):
+    """r = 5 and 7 (ten and twenty-one slot pairs per file)."""
+    q = 2
+    s = oracle.assign(K, r)
+    wl = synth.Workload(0, K, r, q, d, synth.DIST_NORMAL, "weak", "reversed", "fixed")
+    g, _ = synth.generate(wl, s, d=d)
+    _check(g, K, r, q)
+
+
+def test_guess_miss_worker_major():
+    """A worker deviating only after the probe prefix: the fallback runs
+    through the row table as well."""
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = 65536 + 516
+    g, _ = synth.generate(wl, s, d=d)
+    for i in range(s.shape[0]):
+        for x in range(wl.r):
+            if s[i, x] == 5:
+                g.view(np.uint32)[i, x, d - 3] ^= np.uint32(0x10)
+    b, _ = _check(g, wl.K, wl.r, wl.q)
+    assert b["stats"]["fused"] == 1 and b["stats"]["speculation_hit"] == 0
+
+
+def test_shape_checked():
+    import torch
+    wl = synth.WORKLOADS[1]
+    bad = torch.zeros((wl.K, 3, 8), dtype=torch.float32, device=device())
+    with pytest.raises(aspis.AspisError):
+        aspis.detect_aggregate(bad, wl.K, wl.r, wl.q, layout="worker")
