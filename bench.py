@@ -111,7 +111,8 @@ def simulate_tables() -> int:
                 "epsilon_baseline": round(res["epsilon_baseline"], 6),
                 "epsilon_detox": None if det is None else round(det, 6),
                 "success": res["success"], "omega": res["omega"],
-                "n_maximum": res["n_maximum"], "ms_clique": round(res["ms_clique"], 4),
+                "n_maximum": res["n_maximum"], "n_maximal": res["n_maximal"],
+                "ms_clique": round(res["ms_clique"], 4),
                 "ms_files": round(res["ms_files"], 3), "ms_wall": round(wall, 3)}
 
     tables = [row(K, 3, q, a) for K, qmax in ((15, 7), (21, 10), (24, 11))
