@@ -381,8 +381,8 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         row_of = ws.row_of;
     }
 
-    const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) && mode != ASPIS_REDUCE_MEAN &&
-                           aspis::fused_supported(f, r);
+    const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) &&
+                           (aspis::fused_supported(f, r) || aspis::fused_mean_supported(f, r));
     if (try_fused) {
         // 1) agreement on a coordinate prefix -> provisional clique and selection
         const int64_t probe = d < (int64_t(1) << 16) ? d : (int64_t(1) << 16);
@@ -396,21 +396,28 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
         aspis_clique_result guess{};
         if ((st = graph_to_host(&guess)) != ASPIS_OK) { destroy(); return st; }
-        if (!use_mean(mode, &guess)) {
+        // the reduction the guess calls for: the median (Case 2, or MEDIAN
+        // mode) or the mean (Case 1 in PAPER mode, or MEAN mode)
+        const bool guess_mean = use_mean(mode, &guess);
+        if (guess_mean ? aspis::fused_mean_supported(f, r) : aspis::fused_supported(f, r)) {
             local.fused = 1;
             ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, guess.success,
                                            honest_mask(&guess), row_of, ws, false, nullptr, s));
-            // 2) one pass: agreement on every coordinate + median with the guess
+            // 2) one pass: agreement on every coordinate + the reduction with
+            //    the guessed selection
             ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
-            ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
+            if (guess_mean)
+                ASPIS_HIP(aspis::launch_fused_mean(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
+            else
+                ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
             ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
             ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote,
                                          det->has_majority, det->disagree, s));
             if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
             // 3) the final selection; the guess holds iff it selected the same
-            //    replica of every file and the reduction is still the median
+            //    replica of every file and calls for the same reduction
             const int64_t m = kept_files(K, r, f, res);
             if (n_selected) *n_selected = m;
             ASPIS_HIP(aspis::launch_fill_u32(reinterpret_cast<uint32_t *>(ws.flag), 1, 0u, s));
@@ -420,7 +427,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             int32_t flag = 0;
             ASPIS_HIP(hipMemcpyAsync(&flag, ws.flag, sizeof flag, hipMemcpyDeviceToHost, s));
             ASPIS_HIP(hipStreamSynchronize(s));
-            const bool hit = flag == 0 && !use_mean(mode, res);
+            const bool hit = flag == 0 && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) { destroy(); return fail(ASPIS_ERR_NO_FILES, "selection kept no file"); }
             if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));

@@ -77,6 +77,14 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
                         hipStream_t s);
 bool fused_supported(int64_t f, int r);
 
+// Single pass with the mean: agreement bits of every file over [0, d) and
+// the fp64 mean of the rows selected by ws (a guess).
+constexpr int64_t kFusedMeanLds = 64 * 1024;   // per-file words in LDS
+hipError_t launch_fused_mean(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                             const Workspace &ws, uint32_t *pair_diff, float *out,
+                             hipStream_t s);
+bool fused_mean_supported(int64_t f, int r);
+
 // Host-visible comparison of two selections (writes 1 to *flag if any
 // entry of a and b differ; the caller zeroes flag).
 hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,

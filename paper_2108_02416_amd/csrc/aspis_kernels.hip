@@ -817,7 +817,92 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
 }
 
 // ---------------------------------------------------------------------------
+// fused agreement + mean (one read of all r replicas): each thread owns four
+// coordinates and walks every file in ascending order, comparing the r
+// replicas and adding the guessed replica to an fp64 sum -- the file order
+// of the sum is the mean kernel's and the oracle's.  A wave reads 1 KiB of
+// one row per load.  The pair-difference bits of a wave are combined with
+// ballots into per-workgroup LDS words, merged into pair_diff at the end.
+
+constexpr int kMeanFiles = 4;   // files per burst of loads (R rows each)
+
+template <int R, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+fused_mean_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
+                  int64_t d, const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
+                  const int32_t *__restrict__ n_sel, uint32_t *__restrict__ pair_diff,
+                  float *__restrict__ out) {
+    extern __shared__ uint32_t pdw[];   // [f]
+    const int tid = threadIdx.x;
+    for (int64_t i = tid; i < f; i += kBlock) pdw[i] = 0u;
+    __syncthreads();
+    const int n = *n_sel;
+    const int64_t nq = (d + 3) / 4;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    // every lane of a workgroup runs the same iterations (the ballots need
+    // whole waves); lanes past the end of the rows read and write nothing
+    for (int64_t q0 = (int64_t)blockIdx.x * kBlock; q0 < nq; q0 += stride) {
+        const int64_t k = (q0 + tid) * 4;
+        const int64_t kend = q0 + tid < nq ? d : 0;
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int64_t ib = 0; ib < f; ib += kMeanFiles) {
+            uint32_t v[kMeanFiles][R][4];
+#pragma unroll
+            for (int b = 0; b < kMeanFiles; ++b) {
+                const int64_t i = ib + b;
+                if (i < f) {
+#pragma unroll
+                    for (int s = 0; s < R; ++s)
+                        load4<VEC>(g + replica_row(row_of, i, R, s) * d, k, kend, v[b][s]);
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < kMeanFiles; ++b) {
+                const int64_t i = ib + b;
+                if (i >= f) break;
+                uint32_t diff = 0u;
+                int p = 0;
+#pragma unroll
+                for (int s = 0; s < R; ++s)
+#pragma unroll
+                    for (int u = s + 1; u < R; ++u) {
+                        const uint32_t x = (v[b][s][0] ^ v[b][u][0]) | (v[b][s][1] ^ v[b][u][1]) |
+                                           (v[b][s][2] ^ v[b][u][2]) | (v[b][s][3] ^ v[b][u][3]);
+                        diff |= (x != 0u ? 1u : 0u) << p;
+                        ++p;
+                    }
+                uint32_t wdiff = 0u;
+#pragma unroll
+                for (int q = 0; q < R * (R - 1) / 2; ++q)
+                    if (__ballot((diff >> q) & 1u)) wdiff |= 1u << q;
+                if ((tid & 63) == 0 && wdiff) atomicOr(&pdw[i], wdiff);
+                if (pos[i] >= 0) {
+                    const int s_sel = sel[i];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t w = v[b][0][e];
+#pragma unroll
+                        for (int s = 1; s < R; ++s) w = (s_sel == s) ? v[b][s][e] : w;
+                        acc[e] += (double)__uint_as_float(w);
+                    }
+                }
+            }
+        }
+        if (kend != 0 && n > 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (k + e < d) out[k + e] = (float)(acc[e] / (double)n);
+        }
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < f; i += kBlock)
+        if (pdw[i]) atomicOr(&pair_diff[i], pdw[i]);
+}
+
+// ---------------------------------------------------------------------------
 // mean of the kept rows (fp64, file order)
+
+constexpr int kMeanRows = 8;
 
 template <bool VEC>
 __global__ void __launch_bounds__(kBlock)
@@ -831,11 +916,18 @@ mean_kernel(const float *__restrict__ g, int64_t d,
          q += (int64_t)gridDim.x * blockDim.x) {
         const int64_t k = q * 4;
         double acc[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int j = 0; j < n; ++j) {
-            uint32_t v[4];
-            load4<VEC>(g + (int64_t)rows[j] * d, k, d, v);
+        // bursts of kMeanRows loads, then the additions in row order
+        for (int j0 = 0; j0 < n; j0 += kMeanRows) {
+            uint32_t v[kMeanRows][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc[e] += (double)__uint_as_float(v[e]);
+            for (int b = 0; b < kMeanRows; ++b)
+                if (j0 + b < n) load4<VEC>(g + (int64_t)rows[j0 + b] * d, k, d, v[b]);
+#pragma unroll
+            for (int b = 0; b < kMeanRows; ++b)
+                if (j0 + b < n) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[e] += (double)__uint_as_float(v[b][e]);
+                }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -1106,6 +1198,35 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     }
 #undef ASPIS_FUSED_R
 #undef ASPIS_FUSED
+    return hipGetLastError();
+}
+
+bool fused_mean_supported(int64_t f, int r) {
+    return (r == 3 || r == 5 || r == 7) && f * 4 <= kFusedMeanLds;
+}
+
+hipError_t launch_fused_mean(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                             const Workspace &ws, uint32_t *pair_diff, float *out,
+                             hipStream_t s) {
+    if (!fused_mean_supported(f, r)) return hipErrorInvalidValue;
+    const int64_t nq = (d + 3) / 4;
+    const unsigned grid = (unsigned)grid_for((nq + kBlock - 1) / kBlock, (int64_t)num_cus() * 4);
+    const size_t lds = (size_t)f * 4;
+    const bool vec = (d % 4 == 0) && aligned16(g);
+#define ASPIS_FMEAN(RR)                                                                      \
+    if (vec)                                                                                 \
+        fused_mean_kernel<RR, true><<<grid, kBlock, lds, s>>>(g, row_of, f, d, ws.sel,       \
+                                                              ws.pos, ws.n_sel, pair_diff, out); \
+    else                                                                                     \
+        fused_mean_kernel<RR, false><<<grid, kBlock, lds, s>>>(g, row_of, f, d, ws.sel,      \
+                                                               ws.pos, ws.n_sel, pair_diff, out);
+    switch (r) {
+    case 3: ASPIS_FMEAN(3) break;
+    case 5: ASPIS_FMEAN(5) break;
+    case 7: ASPIS_FMEAN(7) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_FMEAN
     return hipGetLastError();
 }
 

@@ -72,6 +72,36 @@ def test_workloads_small_modes(idx, mode):
     _check(g, wl.K, wl.r, wl.q, mode, "two_pass")
 
 
+@pytest.mark.parametrize("mode", ["mean", "paper"])
+@pytest.mark.parametrize("idx", [1, 2, 4])
+def test_fused_mean_runs_single_pass(idx, mode):
+    """On workloads whose detection succeeds, PAPER (and MEAN) reduce by the
+    mean of Algorithm 1 Case 1, in one read like the median."""
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D4[idx] + 3)
+    got, ref = _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    assert ref["clique"]["success"]
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 1
+
+
+@pytest.mark.parametrize("mode", ["mean", "paper"])
+def test_fused_mean_guess_corrected(mode):
+    """A worker deviating only after the probe prefix: the mean computed with
+    the guessed selection is redone with the final one (PAPER also switches
+    from the mean to the median when detection fails in the end)."""
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = 65536 + 778
+    g, _ = synth.generate(wl, s, d=d)
+    for i in range(s.shape[0]):
+        for x in range(wl.r):
+            if s[i, x] == 5:
+                g.view(np.uint32)[i, x, d - 5] ^= np.uint32(0x100)
+    got, _ = _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+
+
 _SPECIAL = np.array([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 3.4e38, -3.4e38],
                     dtype=np.float32)
 _NANS = np.array([0x7FC00000, 0x7FC00001, 0xFFC00000, 0x7F800001, 0xFFFFFFFF],
