@@ -1,29 +1,33 @@
 // aspis_kernels.hip -- gfx950 kernels of the Aspis detect-and-aggregate step.
 //
-// The replica tensor is float32 [f][r][d]: row (i,s) holds the gradient the
-// worker in slot s returned for file i.  Everything here is integer work on
-// the 32-bit patterns (bitwise comparison, order-preserving keys) except the
-// fp64 sums of the mean, so nothing is a dense contraction and no MFMA is
-// used; the kernels are bound by HBM reads.
+// The replicas are float32 rows of d coordinates: row (i,s) holds the
+// gradient the worker in slot s returned for file i, either at row i*r+s of
+// a file-major [f][r][d] tensor or through a row table (the workers' own
+// [K][l][d] uploads).  Everything here is integer work on the 32-bit
+// patterns (bitwise comparison, order-preserving keys) except the fp64 sums
+// of the mean, so nothing is a dense contraction and no MFMA is used; the
+// kernels are bound by HBM reads.
 //
-//   agree_kernel   Eq. (4): per file, OR over coordinates of "slot pair p
-//                  differs"; one coalesced stream over the r rows of a file.
-//   vote_kernel    Eq. (3) majority per file and the K x K disagreement rows
-//                  (Section 4: edge iff the pair agrees on all common files).
-//   select_kernel  Algorithm 1 selection (Case 1 honest replica / Case 2
-//                  majority) and the ordered list of kept rows.
-//   median_kernel  Algorithm 1 Case 2 coordinate-wise median: a tile of T
-//                  coordinates x all kept rows is staged in LDS as totalOrder
-//                  keys, then each column's lower median is found by an MSB
-//                  radix select run by G = BLOCK/T lanes of one wave.
-//   fused_kernel   agree + median in one read: streams all r replicas of a
-//                  tile, compares them, and stages the guessed selection.
-//   mean_kernel    Algorithm 1 Case 1 mean, fp64 accumulation in file order.
-//
-// The tile kernels run one 1024-thread workgroup per CU (16 waves; 512 or
-// 256 threads for the narrow tiles), issue each batch of row loads as a
-// burst before using any of them, and read the LDS tile in batches of eight
-// during the selection, so that neither phase is bound by latency.
+//   agree_kernel       Eq. (4): per file, OR over coordinates of "slot pair p
+//                      differs"; one coalesced stream over the r rows.
+//   vote_kernel        Eq. (3) majority per file and the K x K disagreement
+//                      rows (Section 4: edge iff the pair agrees on all
+//                      common files).
+//   select_kernel      Algorithm 1 selection (Case 1 honest replica / Case 2
+//                      majority) and the ordered list of kept rows.
+//   median_kernel      Algorithm 1 Case 2 coordinate-wise median: a tile of T
+//                      coordinates x all kept rows is staged in LDS as
+//                      totalOrder keys, and each column's lower median is
+//                      found by G lanes of one wave (select_tile: one LDS
+//                      histogram round, then a bitwise radix finish).
+//   fused_ws_kernel    agreement + median in one read, warp-specialised: half
+//                      of the waves stream the next tile while the other half
+//                      select on the current one (the headline path, r = 3).
+//   fused_kernel       agreement + median in one read for r = 5, 7 and
+//                      unaligned rows (load, then select, per tile).
+//   fused_mean_kernel  agreement + Case 1 mean in one read.
+//   mean_kernel        Algorithm 1 Case 1 mean, fp64 accumulation in file
+//                      order.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
