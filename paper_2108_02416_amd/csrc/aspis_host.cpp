@@ -347,7 +347,8 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f, r));
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-    if (mode != ASPIS_REDUCE_MEAN && aspis::pick_median_tile(f) == 0)
+    // PAPER needs the median only when detection fails: checked once known
+    if (mode == ASPIS_REDUCE_MEDIAN && aspis::pick_median_tile(f) == 0)
         return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
                     (long long)aspis::median_capacity(4));
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -430,6 +431,11 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             const bool hit = flag == 0 && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) { destroy(); return fail(ASPIS_ERR_NO_FILES, "selection kept no file"); }
+            if (!hit && !use_mean(mode, res) && aspis::pick_median_tile(f) == 0) {
+                destroy();
+                return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
+                            (long long)aspis::median_capacity(4));
+            }
             if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
             if (!hit) {
                 // ws.pos / ws.rows / ws.n_sel now describe the final selection

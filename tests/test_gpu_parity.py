@@ -102,6 +102,23 @@ def test_fused_mean_guess_corrected(mode):
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
 
 
+def test_many_files_paper_mode():
+    """f = C(41,3) = 10,660 files is past what the LDS median tile holds but
+    not past the single-pass mean: PAPER mode (detection succeeds, so the
+    mean) works, MEDIAN mode is refused with INVALID_ARG."""
+    K, r, q, d = 41, 3, 3, 96
+    s = oracle.assign(K, r)
+    wl = synth.Workload(0, K, r, q, d, synth.DIST_NORMAL, "weak", "reversed", "fixed")
+    g, _ = synth.generate(wl, s, d=d)
+    got, ref = _check(g, K, r, q, "paper", "fused")
+    assert ref["clique"]["success"] and got["stats"]["fused"] == 1
+    import torch
+    gd = torch.from_numpy(g).to(device())
+    with pytest.raises(aspis.AspisError) as e:
+        aspis.detect_aggregate(gd, K, r, q, mode="median")
+    assert e.value.status == aspis.ERR_INVALID_ARG
+
+
 _SPECIAL = np.array([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 3.4e38, -3.4e38],
                     dtype=np.float32)
 _NANS = np.array([0x7FC00000, 0x7FC00001, 0xFFC00000, 0x7F800001, 0xFFFFFFFF],
