@@ -821,6 +821,100 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
 }
 
 // ---------------------------------------------------------------------------
+// median of the kept rows, warp-specialised like fused_ws_kernel: waves 0-7
+// stream the kept rows of tile t+1 (one row per kept file, through the row
+// list of the selection) into registers while waves 8-15 select on tile t.
+// Used by the two-pass path and after a wrong guess of the single pass.
+
+template <int SW>
+constexpr int mws_batch() { return SW >= 16 ? 4 : (SW < 6 ? SW : 6); }
+
+template <int T, int SW>
+__global__ void __launch_bounds__(kWsFill + kWsSelect)
+median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
+                 const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
+    extern __shared__ uint32_t smem[];
+    constexpr int G = kWsSelect / T;     // selection lanes per column
+    constexpr int CPR = T / 4;           // float4 chunks per row segment
+    constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
+    constexpr int B = mws_batch<SW>();   // sweeps per burst of loads
+    const int n = *n_sel;
+    if (n <= 0) return;                  // uniform: no workgroup reaches a barrier
+    uint32_t *hist = smem;
+    uint32_t *tile = smem + hist_words(T);
+    int32_t *rl = reinterpret_cast<int32_t *>(tile + (int64_t)n * T);   // [n] kept rows
+    const int tid = threadIdx.x;
+    for (int i = tid; i < n; i += kWsFill + kWsSelect) rl[i] = rows[i];
+    for (int i = tid; i < hist_words(T); i += kWsFill + kWsSelect) hist[i] = 0u;
+    __syncthreads();
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (wave < kWsFill / 64) {
+        const int cq = tid % CPR, j0 = tid / CPR;
+        uint32_t keys[SW][4];
+        // one 16-byte chunk of kept row j (a lane past the last kept row
+        // re-reads row 0, which is never put; past the end of the rows it
+        // re-reads the row's last chunk, whose median is never written)
+        auto load_row = [&](int64_t t, int x) __attribute__((always_inline)) {
+            const int64_t col = min(t * T + 4 * cq, d - 4);
+            const int j = j0 + x * RPI < n ? j0 + x * RPI : 0;
+            return *reinterpret_cast<const uint4 *>(g + (int64_t)rl[j] * d + col);
+        };
+        auto to_keys = [&](int x, uint4 q) __attribute__((always_inline)) {
+            keys[x][0] = to_key(q.x);
+            keys[x][1] = to_key(q.y);
+            keys[x][2] = to_key(q.z);
+            keys[x][3] = to_key(q.w);
+        };
+        uint4 c0;   // sweep 0 of the next tile, loaded early
+        auto stream_rest = [&](int64_t t) __attribute__((always_inline)) {
+            to_keys(0, c0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int xb = 1; xb < SW; xb += B) {
+                uint4 c[B];
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    if (xb + b < SW) c[b] = load_row(t, xb + b);
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    if (xb + b < SW) to_keys(xb + b, c[b]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        auto put_tile = [&]() __attribute__((always_inline)) {
+#pragma unroll
+            for (int x = 0; x < SW; ++x) {
+                const int j = j0 + x * RPI;
+                if (j < n) put_keys<T, G>(tile, j, cq, keys[x]);
+            }
+        };
+        int64_t t = blockIdx.x;
+        if (t < ntiles) {
+            c0 = load_row(t, 0);
+            stream_rest(t);
+        }
+        if (t + gridDim.x < ntiles) c0 = load_row(t + gridDim.x, 0);
+        if (t < ntiles) put_tile();
+        __syncthreads();
+        for (; t < ntiles; t += gridDim.x) {
+            const int64_t tn = t + gridDim.x;
+            if (tn < ntiles) stream_rest(tn);
+            if (tn + gridDim.x < ntiles) c0 = load_row(tn + gridDim.x, 0);
+            __syncthreads();
+            if (tn < ntiles) put_tile();
+            __syncthreads();
+        }
+    } else {
+        __syncthreads();
+        for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+            select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+            __syncthreads();
+            __syncthreads();
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // fused agreement + mean (one read of all r replicas): each thread owns four
 // coordinates and walks every file in ascending order, comparing the r
 // replicas and adding the guessed replica to an fp64 sum -- the file order
@@ -1076,8 +1170,65 @@ hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
     return hipGetLastError();
 }
 
+// Warp-specialised median: widest tile whose key block, histograms and row
+// list fit in LDS for up to f kept rows, at most 16 sweeps.
+struct MwsPlan {
+    int T = 0;
+    int sweeps = 0;
+};
+
+MwsPlan mws_plan(int64_t f, bool vec) {
+    MwsPlan p;
+    if (!vec) return p;
+    for (int T : {64, 32, 16, 8}) {
+        if (hist_words(T) * 4 + f * 4 * (int64_t)T + f * 4 > kLdsBytes) continue;
+        const int64_t rpi = kWsFill / (T / 4);
+        const int64_t sw = (f + rpi - 1) / rpi;
+        // 16 sweeps fit the registers only next to the 64-column selection
+        if (sw > (T == 64 ? 16 : 12)) continue;
+        p.T = T;
+        p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
+        return p;
+    }
+    return p;
+}
+
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
                          float *out, hipStream_t s) {
+    const bool vec_ws = (d % 4 == 0) && aligned16(g);
+    const MwsPlan plan = mws_plan(f, vec_ws);
+    if (plan.T != 0) {
+        const int T = plan.T;
+        const int64_t ntiles = (d + T - 1) / T;
+        const size_t lds = (size_t)(hist_words(T) * 4 + f * 4 * T + f * 4);
+        const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
+#define ASPIS_MWS(TT, SWW)                                                                   \
+    median_ws_kernel<TT, SWW><<<grid, kWsFill + kWsSelect, lds, s>>>(g, d, ws.rows, ws.n_sel, \
+                                                                     ntiles, out);
+#define ASPIS_MWS_T(TT)                            \
+    switch (plan.sweeps) {                         \
+    case 4: ASPIS_MWS(TT, 4) break;                \
+    case 8: ASPIS_MWS(TT, 8) break;                \
+    case 12: ASPIS_MWS(TT, 12) break;              \
+    default: return hipErrorInvalidValue;          \
+    }
+        switch (T) {
+        case 64:
+            if (plan.sweeps == 16) {
+                ASPIS_MWS(64, 16)
+            } else {
+                ASPIS_MWS_T(64)
+            }
+            break;
+        case 32: ASPIS_MWS_T(32) break;
+        case 16: ASPIS_MWS_T(16) break;
+        case 8: ASPIS_MWS_T(8) break;
+        default: return hipErrorInvalidValue;
+        }
+#undef ASPIS_MWS_T
+#undef ASPIS_MWS
+        return hipGetLastError();
+    }
     const int T = pick_tile(f, 0);
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
