@@ -124,3 +124,25 @@ def test_device_entry_points_validate_before_touching_the_gpu():
     assert L.aspis_detect(None, 7, 3, 10, 16, ctypes.byref(det), None) == aspis.ERR_INVALID_ARG
     assert L.aspis_aggregate_workspace(7, 3, 10) >= 35 * 12
     assert L.aspis_aggregate_workspace(7, 2, 10) == 0
+
+
+def test_worker_major_entry_validates_before_touching_the_gpu():
+    L = aspis.lib()
+    det = aspis.DetectOut(1, 1, 1, 1)
+    res = aspis.CliqueResult()
+    n = ctypes.c_int64(0)
+    stats = aspis.RunStats()
+
+    def call(grads, K, r, q, d, ws_bytes=1 << 20, ws=256):
+        return L.aspis_detect_aggregate_wm(grads, K, r, q, d, 16, ctypes.byref(det), 0, 16, None,
+                                           ctypes.byref(res), ctypes.byref(n), ws, ws_bytes, 0,
+                                           ctypes.byref(stats), None)
+    assert call(16, 7, 4, 2, 10) == aspis.ERR_INVALID_ARG        # even r
+    assert call(16, 7, 3, 4, 10) == aspis.ERR_INVALID_ARG        # q >= K/2
+    assert call(16, 7, 3, 2, 0) == aspis.ERR_INVALID_ARG         # d = 0
+    assert call(None, 7, 3, 2, 10) == aspis.ERR_INVALID_ARG      # NULL replicas
+    assert call(16, 7, 3, 2, 10, ws_bytes=64) == aspis.ERR_BUFFER_SMALL
+    assert call(16, 7, 3, 2, 10, ws=257) == aspis.ERR_INVALID_ARG  # unaligned workspace
+    # the workspace covers the f*r row table of the worker-major layout
+    f, r = 35, 3
+    assert L.aspis_aggregate_workspace(7, 3, 10) >= 4 * f * 4 + f * r * 4
