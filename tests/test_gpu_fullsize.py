@@ -70,3 +70,38 @@ def test_fullsize_workload(idx):
          f"(omega={cl['omega']}, max cliques={cl['n_maximum']}, success={cl['success']})")
     del gd
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("idx", [3])
+def test_fullsize_worker_major_matches_file_major(idx):
+    """The workers' [K][l][d] upload of the headline workload gives the same
+    bits as the file-major tensor (which test_fullsize_workload checks
+    against the oracle): detection, selection and every median."""
+    import torch
+    wl = synth.WORKLOADS[idx]
+    K, r, q, d, f = wl.K, wl.r, wl.q, wl.d, wl.f
+    s = oracle.assign(K, r)
+    role, worker, A, D = synth.make_roles(wl, s)
+    _log(f"workload {idx}: file-major and worker-major, {2 * wl.replica_bytes() / 1e9:.1f} GB")
+    dev = device()
+    fm = torch.empty((f, r, d), dtype=torch.float32, device=dev)
+    synth.fill_device(role, worker, fm, wl.dist, alie_z=wl.alie_z)
+    a = aspis.detect_aggregate(fm, K, r, q, flags=aspis.FLAG_TIMING)
+    l_files = f * r // K
+    rows = torch.from_numpy(aspis.worker_rows(K, r).reshape(-1).astype(np.int64)).to(dev)
+    wm = torch.empty((K * l_files, d), dtype=torch.float32, device=dev)
+    wm.index_copy_(0, rows, fm.view(f * r, d))
+    del fm
+    torch.cuda.synchronize()
+    b = aspis.detect_aggregate(wm.view(K, l_files, d), K, r, q, flags=aspis.FLAG_TIMING,
+                               layout="worker")
+    torch.cuda.synchronize()
+    _log(f"file-major {a['stats']}, worker-major {b['stats']}")
+    assert b["stats"]["fused"] == 1
+    assert np.array_equal(to_np(a["bufs"].pair_diff), to_np(b["bufs"].pair_diff))
+    assert np.array_equal(to_np(a["bufs"].vote), to_np(b["bufs"].vote))
+    assert np.array_equal(to_np(a["sel"]), to_np(b["sel"]))
+    assert a["n_selected"] == b["n_selected"]
+    assert np.array_equal(to_np(a["out"]).view(np.uint32), to_np(b["out"]).view(np.uint32))
+    del wm
+    torch.cuda.empty_cache()
