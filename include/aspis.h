@@ -166,6 +166,10 @@ typedef struct {
     float ms_main;             /* main pass (fused, or detect + reduce)     */
     float ms_fallback;         /* reduction rerun after a wrong guess       */
     float ms_total;            /* first kernel to result, host steps incl.  */
+    int32_t tile_cols;         /* coordinates per tile of the median kernel
+                                  that produced out (0: the mean)          */
+    int32_t half_keys;         /* 1 if that tile held only the high 16 bits
+                                  of each key (low halves read back)       */
 } aspis_run_stats;
 
 #define ASPIS_FLAG_TWO_PASS 1u   /* force detect, clique, then aggregate    */

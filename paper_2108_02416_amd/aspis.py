@@ -77,7 +77,8 @@ class RunStats(ctypes.Structure):
     _fields_ = [("fused", ctypes.c_int32), ("speculation_hit", ctypes.c_int32),
                 ("probe_coords", ctypes.c_int64), ("ms_probe", ctypes.c_float),
                 ("ms_main", ctypes.c_float), ("ms_fallback", ctypes.c_float),
-                ("ms_total", ctypes.c_float)]
+                ("ms_total", ctypes.c_float), ("tile_cols", ctypes.c_int32),
+                ("half_keys", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -294,7 +294,7 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
                             int64_t d, const int32_t *subsets_dev, const aspis_detect_out *det,
                             const aspis_clique_result *res, aspis_reduce mode, float *out,
                             int32_t *sel_out, int64_t *n_selected, void *workspace,
-                            size_t ws_bytes, void *stream) {
+                            size_t ws_bytes, void *stream, aspis::TileUse *use = nullptr) {
     int64_t f = 0;
     aspis_status st = check_device_shape(K, r, d, &f);
     if (st != ASPIS_OK) return st;
@@ -322,7 +322,7 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
     if (mean)
         ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
     else
-        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s));
+        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, use));
     return ASPIS_OK;
 }
 
@@ -402,6 +402,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         const bool guess_mean = use_mean(mode, &guess);
         if (guess_mean ? aspis::fused_mean_supported(f, r) : aspis::fused_supported(f, r)) {
             local.fused = 1;
+            aspis::TileUse fused_tile{};   // stays empty for the mean
             ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, guess.success,
                                            honest_mask(&guess), row_of, ws, false, nullptr, s));
             // 2) one pass: agreement on every coordinate + the reduction with
@@ -411,7 +412,8 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             if (guess_mean)
                 ASPIS_HIP(aspis::launch_fused_mean(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
             else
-                ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
+                ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s,
+                                              &fused_tile));
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
             ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
             ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote,
@@ -439,11 +441,14 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
             if (!hit) {
                 // ws.pos / ws.rows / ws.n_sel now describe the final selection
+                fused_tile = aspis::TileUse{};
                 if (use_mean(mode, res))
                     ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
                 else
-                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s));
+                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile));
             }
+            local.tile_cols = fused_tile.cols;
+            local.half_keys = fused_tile.half;
             if (timing) ASPIS_HIP(hipEventRecord(ev[5], s));
             ASPIS_HIP(hipStreamSynchronize(s));
             if (timing) {
@@ -464,8 +469,11 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         return st;
     }
     if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
+    aspis::TileUse tile{};
     st = aggregate_impl(grads, row_of, K, r, d, subsets_dev, det, res, mode, out, sel_out,
-                        n_selected, workspace, ws_bytes, stream);
+                        n_selected, workspace, ws_bytes, stream, &tile);
+    local.tile_cols = tile.cols;
+    local.half_keys = tile.half;
     if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
     ASPIS_HIP(hipStreamSynchronize(s));
     if (timing) ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));

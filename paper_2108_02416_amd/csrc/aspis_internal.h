@@ -64,9 +64,16 @@ hipError_t launch_select(const int32_t *subsets, const int8_t *vote,
 // Tile width the median kernel uses for up to f kept files (0: too many).
 int pick_median_tile(int64_t f);
 
+// Tile a median kernel ran with: columns per tile, and whether the tile
+// kept only the high halves of the keys.
+struct TileUse {
+    int32_t cols = 0;
+    int32_t half = 0;
+};
+
 // Coordinate-wise lower median / fp64 mean of the kept rows.
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,
-                         int64_t f, float *out, hipStream_t s);
+                         int64_t f, float *out, hipStream_t s, TileUse *use = nullptr);
 hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
                        float *out, hipStream_t s);
 
@@ -74,7 +81,7 @@ hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
 // the rows selected by ws (a guess), in one read of the replica tensor.
 hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         const Workspace &ws, uint32_t *pair_diff, float *out,
-                        hipStream_t s);
+                        hipStream_t s, TileUse *use = nullptr);
 bool fused_supported(int64_t f, int r);
 
 // Single pass with the mean: agreement bits of every file over [0, d) and

@@ -113,7 +113,7 @@ constexpr int tile_block() { return T >= 16 ? 1024 : 64 * T; }
 // lanes of every half-wave in 32 distinct banks.
 template <int T, int G>
 __device__ __forceinline__ int tile_swz(int g) {
-    static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64, "tile width");
+    static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64 || T == 128, "tile width");
     static_assert(G >= 1 && G <= 64 && (G & (G - 1)) == 0, "lanes per column");
     if constexpr (T >= 32) {
         static_assert(G <= 32, "swizzle needs at most 32 lanes per wide column");
@@ -336,6 +336,233 @@ __device__ __forceinline__ void select_tile(uint32_t *tile, uint32_t *hist, int 
         varying = a ^ o;
     }
     if (g == 0 && k0 + c < d) out[k0 + c] = __uint_as_float(from_key(a));
+}
+
+// ---------------------------------------------------------------------------
+// Half-key tiles.  The LDS tile holds only the high 16 bits of every key,
+// two rows per word, so a tile of the same LDS size is twice as wide (and
+// the row segments read from HBM twice as long).  The high half of the
+// sought key is selected exactly on the tile; the low halves are then read
+// back from the replica rows, only for the rows whose high half equals it
+// (about one row per column on continuous data; every row when all high
+// halves of a column are equal, which costs speed, not exactness).
+//
+// Layout: row j sits in pair-row p = j / 2, in the low (j even) or high
+// (j odd) half of word p*T + (c ^ swz(p % G)).  For an odd row count the
+// high half of the last word is unused and never read.
+
+constexpr int kHalfWindow = 6;                  // key bits per histogram round
+constexpr int kHalfBuckets = 1 << kHalfWindow;
+constexpr int kHalfStride = kHalfBuckets + 4;   // words per column block (16-byte aligned)
+
+__host__ __device__ constexpr int64_t half_hist_words(int T) { return (int64_t)T * kHalfStride; }
+__host__ __device__ constexpr int64_t half_tile_words(int64_t rows, int T) {
+    return (rows + 1) / 2 * T;
+}
+
+// Store the high key halves of row j, columns 4cq..4cq+3 (lo2: columns 0,1;
+// hi2: columns 2,3, each column's half in the low 16 bits first).
+template <int T, int G>
+__device__ __forceinline__ void put_half(uint32_t *tile, int j, int cq, uint32_t lo2, uint32_t hi2) {
+    const int p = j >> 1;
+    const int sw = tile_swz<T, G>(p % G);
+    uint16_t *row = reinterpret_cast<uint16_t *>(tile + p * T) + (j & 1);
+    row[2 * ((4 * cq + 0) ^ sw)] = (uint16_t)lo2;
+    row[2 * ((4 * cq + 1) ^ sw)] = (uint16_t)(lo2 >> 16);
+    row[2 * ((4 * cq + 2) ^ sw)] = (uint16_t)hi2;
+    row[2 * ((4 * cq + 3) ^ sw)] = (uint16_t)(hi2 >> 16);
+}
+
+// The high halves of two full keys, packed (a's in the low 16 bits).
+__device__ __forceinline__ uint32_t pack_high(uint32_t a, uint32_t b) {
+    return (a >> 16) | (b & 0xFFFF0000u);
+}
+
+// Lower median of each of the T columns of a half-key tile of n rows
+// (1 <= n <= 65535), by the G lanes stid = c*G + g of column c, written to
+// out[k0 + c] for k0 + c < d.  Row j of the tile is replica row rows[j] of
+// g (rows may point to global memory or LDS).  hist: half_hist_words(T)
+// words, zero on entry and on exit.  The tile is overwritten.
+//
+//  1. one pass for the common magnitude bits and the count of sign-clear
+//     keys (as in select_tile), which settles the sign;
+//  2. histogram rounds over the 16-bit keys, each resolving kHalfWindow bits
+//     below the last settled one, until the sought high half H is known
+//     (at most 3 rounds); nothing is compacted, every round reads all keys;
+//  3. one pass collecting the rows whose high half is H into the lane's
+//     16-bit slots (in place), then their low halves are read from g;
+//  4. bitwise radix select on those low halves for the remaining rank.
+template <int T, int G>
+__device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist, int n, int64_t k0,
+                                                 int64_t d, float *out, int stid,
+                                                 const float *__restrict__ g,
+                                                 const int32_t *rows) {
+    constexpr int STRIDE = G * T;   // words between a lane's pair-rows
+    constexpr int BPL = kHalfBuckets / G;
+    static_assert(BPL >= 2 && BPL % 2 == 0, "buckets per lane");
+    const int gl = stid % G;
+    const int c = stid / G;
+    uint32_t *base = tile + gl * T + (c ^ tile_swz<T, G>(gl));
+    uint16_t *base16 = reinterpret_cast<uint16_t *>(base);
+    uint32_t *hcol = hist + c * kHalfStride;
+    const int np = (n + 1) >> 1;
+    const int cnt = np > gl ? (np - gl + G - 1) / G : 0;   // words of this lane
+    const bool tail = (n & 1) != 0 && gl == (np - 1) % G;  // its last word holds one row
+    const int full = cnt - (tail ? 1 : 0);
+    uint32_t m = (uint32_t)(n - 1) / 2;
+
+    // every key of the lane: fn(key, word x, half h) for row 2*(gl + x*G) + h
+    auto each = [&](auto &&fn) __attribute__((always_inline)) {
+        int x = 0;
+        for (; x + kSelBatch <= full; x += kSelBatch) {
+            uint32_t v[kSelBatch];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u) {
+                fn(v[u] & 0xFFFFu, x + u, 0);
+                fn(v[u] >> 16, x + u, 1);
+            }
+        }
+        for (; x < full; ++x) {
+            const uint32_t v = base[x * STRIDE];
+            fn(v & 0xFFFFu, x, 0);
+            fn(v >> 16, x, 1);
+        }
+        if (tail) fn(base[full * STRIDE] & 0xFFFFu, full, 0);
+    };
+    // the lane's x-th 16-bit slot (step 3 on)
+    auto slot = [&](int x) __attribute__((always_inline)) -> uint16_t & {
+        return base16[(x >> 1) * 2 * STRIDE + (x & 1)];
+    };
+
+    // 1. common magnitude bits, keys with the top bit clear (negative values)
+    uint32_t am = 0x7FFFu, om = 0u, z = 0u;
+    each([&](uint32_t k, int, int) {
+        const uint32_t mag = (k ^ ((k >> 15) - 1u)) & 0x7FFFu;
+        am &= mag;
+        om |= mag;
+        z += k >> 15;
+    });
+    am = group_reduce<G, Op::And>(am);
+    om = group_reduce<G, Op::Or>(om);
+    z = (uint32_t)n - group_reduce<G, Op::Add>(z);
+
+    uint32_t sgn = 0x8000u;
+    if (m < z) sgn = 0u;
+    else m -= z;
+    const uint32_t vm = am ^ om;
+    uint32_t H;
+    if (vm == 0u) {   // one magnitude: the sign gives the key
+        H = sgn ? (0x8000u | am) : (~am & 0x7FFFu);
+    } else {
+        // 2. the keys of the sign lie in [bias, bias + 2^(hb+1)); each round
+        //    splits the window into buckets of 2^sh keys and keeps the one
+        //    holding rank m
+        int hb = 31 - __clz(vm);
+        const uint32_t hi = 0x7FFFu & ~((2u << hb) - 1u);
+        uint32_t bias = sgn ? (0x8000u | (am & hi)) : (~am & hi);
+        for (int round = 0; round < 3; ++round) {
+            const int sh = hb >= kHalfWindow - 1 ? hb - (kHalfWindow - 1) : 0;
+            const uint32_t span = 2u << hb;
+            each([&](uint32_t k, int, int) {
+                const uint32_t o = k - bias;
+                if (o < span) atomicAdd(&hcol[o >> sh], 1u);
+            });
+            uint32_t h[BPL];
+#pragma unroll
+            for (int q = 0; q < BPL; q += 2) {
+                const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[gl * BPL + q]);
+                h[q] = w2.x;
+                h[q + 1] = w2.y;
+            }
+#pragma unroll
+            for (int q = 0; q < BPL; q += 2)
+                *reinterpret_cast<uint2 *>(&hcol[gl * BPL + q]) = make_uint2(0u, 0u);
+            uint32_t tot = 0u;
+#pragma unroll
+            for (int q = 0; q < BPL; ++q) tot += h[q];
+            uint32_t run = group_scan<G>(tot, gl) - tot;
+            uint32_t le = 0u, below = 0u;
+#pragma unroll
+            for (int q = 0; q < BPL; ++q) {
+                run += h[q];
+                const bool ok = run <= m;
+                le += ok ? 1u : 0u;
+                below = ok ? run : below;
+            }
+            le = group_reduce<G, Op::Add>(le);
+            below = group_reduce<G, Op::Max>(below);
+            m -= below;
+            bias += le << sh;
+            if (sh == 0) break;   // 15 bits: windows 14..9, 8..3, 2..0 at most
+            hb = sh - 1;
+        }
+        H = bias;
+    }
+
+    // 3. rows whose high half is H, as row numbers in the lane's slots (the
+    //    write cursor never passes the read cursor), then their low halves
+    int w = 0;
+    each([&](uint32_t k, int x, int h) {
+        if (k == H) {
+            slot(w) = (uint16_t)(2 * (gl + x * G) + h);
+            ++w;
+        }
+    });
+    const bool valid = k0 + c < d;
+    constexpr int kGather = 4;   // row reads in flight per lane
+    for (int x0 = 0; x0 < w; x0 += kGather) {
+        uint32_t v[kGather];
+#pragma unroll
+        for (int u = 0; u < kGather; ++u) {
+            v[u] = 0u;
+            if (x0 + u < w && valid)
+                v[u] = __float_as_uint(g[(int64_t)rows[slot(x0 + u)] * d + k0 + c]);
+        }
+#pragma unroll
+        for (int u = 0; u < kGather; ++u)
+            if (x0 + u < w) slot(x0 + u) = (uint16_t)(to_key(v[u]) & 0xFFFFu);
+    }
+
+    // 4. bitwise radix select of rank m among the low halves
+    auto and_or = [&](uint32_t &a, uint32_t &o) __attribute__((always_inline)) {
+        a = 0xFFFFu;
+        o = 0u;
+        for (int x = 0; x < w; ++x) {
+            const uint32_t v = slot(x);
+            a &= v;
+            o |= v;
+        }
+        a = group_reduce<G, Op::And>(a);
+        o = group_reduce<G, Op::Or>(o);
+    };
+    uint32_t a, o;
+    and_or(a, o);
+    uint32_t varying = a ^ o;
+    for (int step = 0; varying != 0u && step < 16; ++step) {
+        const uint32_t bit = 1u << (31 - __clz(varying));
+        uint32_t zc = 0u;
+        for (int x = 0; x < w; ++x) zc += (slot(x) & bit) == 0u;
+        zc = group_reduce<G, Op::Add>(zc);
+        uint32_t want;
+        if (m < zc) {
+            want = 0u;
+        } else {
+            want = bit;
+            m -= zc;
+        }
+        int nw = 0;
+        for (int x = 0; x < w; ++x) {
+            const uint16_t v = slot(x);
+            slot(nw) = v;
+            nw += (v & bit) == want ? 1 : 0;
+        }
+        w = nw;
+        and_or(a, o);
+        varying = a ^ o;
+    }
+    if (gl == 0 && valid) out[k0 + c] = __uint_as_float(from_key((H << 16) | a));
 }
 
 // Load four consecutive coordinates [k, k+4) of one row as bit patterns;
@@ -666,21 +893,23 @@ constexpr int kWsSelect = 512;     // threads of the selection role
 template <int R, int SW>
 constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
 
-template <int T, int R, int SW, bool IND>
+template <int T, int R, int SW, bool IND, bool HALF>
 __global__ void __launch_bounds__(kWsFill + kWsSelect)
 fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
                 const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
-                const int32_t *__restrict__ n_sel, int64_t ntiles,
-                uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
+                const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
+                int64_t ntiles, uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
     extern __shared__ uint32_t smem[];
     constexpr int G = kWsSelect / T;     // selection lanes per column
     constexpr int CPR = T / 4;           // float4 chunks per row segment
     constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
     constexpr int B = ws_batch<R, SW>(); // sweeps per burst of loads
+    constexpr int KW = HALF ? 2 : 4;     // key registers per sweep
     const int n = *n_sel;
+    const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
     uint32_t *hist = smem;               // selection histograms
-    uint32_t *tile = smem + hist_words(T);
-    uint32_t *pd = tile + f * T;         // [f] per-workgroup pair-difference bits
+    uint32_t *tile = smem + hwords;
+    uint32_t *pd = tile + (HALF ? half_tile_words(f, T) : f * T);   // [f] pair-difference bits
     int32_t *ps = reinterpret_cast<int32_t *>(pd + f);   // [f] (tile row << 3) | slot, or -1
     int32_t *rt = ps + f;                // [f*R] row table (IND)
     const int tid = threadIdx.x;
@@ -690,7 +919,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     }
     if constexpr (IND)
         for (int64_t i = tid; i < f * R; i += kWsFill + kWsSelect) rt[i] = row_of[i];
-    for (int i = tid; i < hist_words(T); i += kWsFill + kWsSelect) hist[i] = 0u;
+    for (int i = tid; i < hwords; i += kWsFill + kWsSelect) hist[i] = 0u;
     __syncthreads();
     // roles are whole waves: waves 0-7 stream, waves 8-15 select; every wave
     // executes the same number of barriers (1 + 2 per tile)
@@ -698,7 +927,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     if (wave < kWsFill / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
         const int64_t sweep = (int64_t)RPI * R * d;   // elements between sweeps
-        uint32_t keys[SW][4];
+        uint32_t keys[SW][KW];   // full keys, or packed high halves (HALF)
         // the r replica chunks of one sweep, kept in registers (a value
         // type, so that no per-lane indexing can turn it into memory)
         struct Chunks {
@@ -754,10 +983,15 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
 #pragma unroll
                 for (int s = 1; s < R; ++s)
                     if (s_sel == s) w = c.q[s];
-                keys[x][0] = to_key(w.x);
-                keys[x][1] = to_key(w.y);
-                keys[x][2] = to_key(w.z);
-                keys[x][3] = to_key(w.w);
+                if constexpr (HALF) {
+                    keys[x][0] = pack_high(to_key(w.x), to_key(w.y));
+                    keys[x][1] = pack_high(to_key(w.z), to_key(w.w));
+                } else {
+                    keys[x][0] = to_key(w.x);
+                    keys[x][1] = to_key(w.y);
+                    keys[x][2] = to_key(w.z);
+                    keys[x][3] = to_key(w.w);
+                }
             }
         };
         Chunks c0;   // sweep 0 of the next tile, loaded early
@@ -786,7 +1020,12 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                 const int i = j0 + x * RPI;
                 if (i < f) {
                     const int q = ps[i];
-                    if (q >= 0) put_keys<T, G>(tile, q >> 3, cq, keys[x]);
+                    if (q >= 0) {
+                        if constexpr (HALF)
+                            put_half<T, G>(tile, q >> 3, cq, keys[x][0], keys[x][1]);
+                        else
+                            put_keys<T, G>(tile, q >> 3, cq, keys[x]);
+                    }
                 }
             }
         };
@@ -811,7 +1050,12 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     } else {
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (n > 0) select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+            if (n > 0) {
+                if constexpr (HALF)
+                    select_half_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill, g, rows);
+                else
+                    select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+            }
             __syncthreads();
             __syncthreads();
         }
@@ -829,7 +1073,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
 template <int SW>
 constexpr int mws_batch() { return SW >= 16 ? 4 : (SW < 6 ? SW : 6); }
 
-template <int T, int SW>
+template <int T, int SW, bool HALF>
 __global__ void __launch_bounds__(kWsFill + kWsSelect)
 median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
                  const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
@@ -838,19 +1082,22 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
     constexpr int CPR = T / 4;           // float4 chunks per row segment
     constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
     constexpr int B = mws_batch<SW>();   // sweeps per burst of loads
+    constexpr int KW = HALF ? 2 : 4;     // key registers per sweep
     const int n = *n_sel;
     if (n <= 0) return;                  // uniform: no workgroup reaches a barrier
+    const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
     uint32_t *hist = smem;
-    uint32_t *tile = smem + hist_words(T);
-    int32_t *rl = reinterpret_cast<int32_t *>(tile + (int64_t)n * T);   // [n] kept rows
+    uint32_t *tile = smem + hwords;
+    int32_t *rl = reinterpret_cast<int32_t *>(tile + (HALF ? half_tile_words(n, T)
+                                                           : (int64_t)n * T));   // [n] kept rows
     const int tid = threadIdx.x;
     for (int i = tid; i < n; i += kWsFill + kWsSelect) rl[i] = rows[i];
-    for (int i = tid; i < hist_words(T); i += kWsFill + kWsSelect) hist[i] = 0u;
+    for (int i = tid; i < hwords; i += kWsFill + kWsSelect) hist[i] = 0u;
     __syncthreads();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if (wave < kWsFill / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
-        uint32_t keys[SW][4];
+        uint32_t keys[SW][KW];   // full keys, or packed high halves (HALF)
         // one 16-byte chunk of kept row j (a lane past the last kept row
         // re-reads row 0, which is never put; past the end of the rows it
         // re-reads the row's last chunk, whose median is never written)
@@ -860,10 +1107,15 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
             return *reinterpret_cast<const uint4 *>(g + (int64_t)rl[j] * d + col);
         };
         auto to_keys = [&](int x, uint4 q) __attribute__((always_inline)) {
-            keys[x][0] = to_key(q.x);
-            keys[x][1] = to_key(q.y);
-            keys[x][2] = to_key(q.z);
-            keys[x][3] = to_key(q.w);
+            if constexpr (HALF) {
+                keys[x][0] = pack_high(to_key(q.x), to_key(q.y));
+                keys[x][1] = pack_high(to_key(q.z), to_key(q.w));
+            } else {
+                keys[x][0] = to_key(q.x);
+                keys[x][1] = to_key(q.y);
+                keys[x][2] = to_key(q.z);
+                keys[x][3] = to_key(q.w);
+            }
         };
         uint4 c0;   // sweep 0 of the next tile, loaded early
         auto stream_rest = [&](int64_t t) __attribute__((always_inline)) {
@@ -885,7 +1137,12 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
 #pragma unroll
             for (int x = 0; x < SW; ++x) {
                 const int j = j0 + x * RPI;
-                if (j < n) put_keys<T, G>(tile, j, cq, keys[x]);
+                if (j < n) {
+                    if constexpr (HALF)
+                        put_half<T, G>(tile, j, cq, keys[x][0], keys[x][1]);
+                    else
+                        put_keys<T, G>(tile, j, cq, keys[x]);
+                }
             }
         };
         int64_t t = blockIdx.x;
@@ -907,7 +1164,10 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
     } else {
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+            if constexpr (HALF)
+                select_half_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill, g, rl);
+            else
+                select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
             __syncthreads();
             __syncthreads();
         }
@@ -1170,66 +1430,125 @@ hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
     return hipGetLastError();
 }
 
-// Warp-specialised median: widest tile whose key block, histograms and row
-// list fit in LDS for up to f kept rows, at most 16 sweeps.
-struct MwsPlan {
+// Warp-specialised plans.  Full keys: the widest tile (8..64 columns) whose
+// key block fits in LDS and whose rows fit the streaming role's registers
+// (at most 16 sweeps of 4 key registers).  Half keys, for many rows: a wider
+// tile (16..128 columns) with up to 32 sweeps of 2 key registers; taken
+// only when it is wider than the full-key tile, since below kHalfMinRows
+// rows a tile is streamed too quickly to hide the reads of the low halves.
+struct WsPlan {
     int T = 0;
     int sweeps = 0;
+    bool half = false;
 };
 
-MwsPlan mws_plan(int64_t f, bool vec) {
-    MwsPlan p;
+constexpr int64_t kHalfMinRows = 128;
+
+// Sweep counts built for each plan (a sweep past the last row is skipped).
+// Half keys: 8 only for 128 columns, where fewer than 128 rows never take
+// a narrower half-key tile.
+int round_sweeps(int64_t sw, bool half, int T) {
+    if (half) return sw <= 8 && T == 128 ? 8 : sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
+    return sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
+}
+
+// LDS of the warp-specialised median: histograms, key tile, row list.
+int64_t mws_lds_bytes(int64_t f, int T, bool half) {
+    return half ? (half_hist_words(T) + half_tile_words(f, T)) * 4 + f * 4
+                : (hist_words(T) + f * (int64_t)T) * 4 + f * 4;
+}
+
+WsPlan mws_plan(int64_t f, bool vec) {
+    WsPlan p;
     if (!vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (hist_words(T) * 4 + f * 4 * (int64_t)T + f * 4 > kLdsBytes) continue;
+        if (mws_lds_bytes(f, T, false) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         // 16 sweeps fit the registers only next to the 64-column selection
         if (sw > (T == 64 ? 16 : 12)) continue;
         p.T = T;
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
-        return p;
+        break;
     }
+    if (f >= kHalfMinRows && f < 65535)
+        for (int T : {128, 64, 32, 16}) {
+            if (T <= p.T) break;
+            if (mws_lds_bytes(f, T, true) > kLdsBytes) continue;
+            const int64_t rpi = kWsFill / (T / 4);
+            const int64_t sw = (f + rpi - 1) / rpi;
+            if (sw > 32) continue;
+            p.T = T;
+            p.sweeps = round_sweeps(sw, true, T);
+            p.half = true;
+            break;
+        }
     return p;
 }
 
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
-                         float *out, hipStream_t s) {
+                         float *out, hipStream_t s, TileUse *use) {
     const bool vec_ws = (d % 4 == 0) && aligned16(g);
-    const MwsPlan plan = mws_plan(f, vec_ws);
+    const WsPlan plan = mws_plan(f, vec_ws);
+    if (use) *use = TileUse{plan.T, plan.half ? 1 : 0};
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)(hist_words(T) * 4 + f * 4 * T + f * 4);
+        const size_t lds = (size_t)mws_lds_bytes(f, T, plan.half);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_MWS(TT, SWW)                                                                   \
-    median_ws_kernel<TT, SWW><<<grid, kWsFill + kWsSelect, lds, s>>>(g, d, ws.rows, ws.n_sel, \
-                                                                     ntiles, out);
+#define ASPIS_MWS(TT, SWW, HH)                                                               \
+    median_ws_kernel<TT, SWW, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(g, d, ws.rows,      \
+                                                                         ws.n_sel, ntiles, out);
 #define ASPIS_MWS_T(TT)                            \
     switch (plan.sweeps) {                         \
-    case 4: ASPIS_MWS(TT, 4) break;                \
-    case 8: ASPIS_MWS(TT, 8) break;                \
-    case 12: ASPIS_MWS(TT, 12) break;              \
+    case 4: ASPIS_MWS(TT, 4, false) break;         \
+    case 8: ASPIS_MWS(TT, 8, false) break;         \
+    case 12: ASPIS_MWS(TT, 12, false) break;       \
     default: return hipErrorInvalidValue;          \
     }
-        switch (T) {
-        case 64:
-            if (plan.sweeps == 16) {
-                ASPIS_MWS(64, 16)
-            } else {
-                ASPIS_MWS_T(64)
+#define ASPIS_MWS_H(TT)                            \
+    switch (plan.sweeps) {                         \
+    case 16: ASPIS_MWS(TT, 16, true) break;        \
+    case 24: ASPIS_MWS(TT, 24, true) break;        \
+    case 32: ASPIS_MWS(TT, 32, true) break;        \
+    default: return hipErrorInvalidValue;          \
+    }
+        if (plan.half) {
+            switch (T) {
+            case 128:
+                if (plan.sweeps == 8) {
+                    ASPIS_MWS(128, 8, true)
+                } else {
+                    ASPIS_MWS_H(128)
+                }
+                break;
+            case 64: ASPIS_MWS_H(64) break;
+            case 32: ASPIS_MWS_H(32) break;
+            case 16: ASPIS_MWS_H(16) break;
+            default: return hipErrorInvalidValue;
             }
-            break;
-        case 32: ASPIS_MWS_T(32) break;
-        case 16: ASPIS_MWS_T(16) break;
-        case 8: ASPIS_MWS_T(8) break;
-        default: return hipErrorInvalidValue;
+        } else {
+            switch (T) {
+            case 64:
+                if (plan.sweeps == 16) {
+                    ASPIS_MWS(64, 16, false)
+                } else {
+                    ASPIS_MWS_T(64)
+                }
+                break;
+            case 32: ASPIS_MWS_T(32) break;
+            case 16: ASPIS_MWS_T(16) break;
+            case 8: ASPIS_MWS_T(8) break;
+            default: return hipErrorInvalidValue;
+            }
         }
+#undef ASPIS_MWS_H
 #undef ASPIS_MWS_T
 #undef ASPIS_MWS
         return hipGetLastError();
     }
     const int T = pick_tile(f, 0);
+    if (use) *use = TileUse{T, 0};
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)(f * 4 * T + hist_words(T) * 4);
@@ -1254,32 +1573,40 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     return hipGetLastError();
 }
 
-// Warp-specialised single pass: widest tile (>= 8 columns) whose key block
-// and pair-difference words fit in LDS and whose rows fit the streaming
-// role's register budget (at most 16 sweeps of 512 threads).
-struct WsPlan {
-    int T = 0;
-    int sweeps = 0;
-};
-
-// LDS of the warp-specialised kernel: histograms, key tile, per-file words
-// and, with a row table, the table.
-int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind) {
-    return hist_words(T) * 4 + f * 4 * (int64_t)T + f * 8 + (ind ? f * r * 4 : 0);
+// LDS of the warp-specialised single pass: histograms, key tile, per-file
+// words and, with a row table, the table.
+int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind, bool half) {
+    const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T)
+                               : hist_words(T) + f * (int64_t)T;
+    return words * 4 + f * 8 + (ind ? f * r * 4 : 0);
 }
 
+// Warp-specialised single pass (r = 3, 16-byte aligned rows): plans as for
+// the median above.
 WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     WsPlan p;
     if (r != 3 || !vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (ws_lds_bytes(f, r, T, ind) > kLdsBytes) continue;
+        if (ws_lds_bytes(f, r, T, ind, false) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         if (sw > 16) continue;
         p.T = T;
-        p.sweeps = sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
-        return p;
+        p.sweeps = round_sweeps(sw, false, T);
+        break;
     }
+    if (f >= kHalfMinRows && f < 65535)
+        for (int T : {128, 64, 32, 16}) {
+            if (T <= p.T) break;
+            if (ws_lds_bytes(f, r, T, ind, true) > kLdsBytes) continue;
+            const int64_t rpi = kWsFill / (T / 4);
+            const int64_t sw = (f + rpi - 1) / rpi;
+            if (sw > 32) continue;
+            p.T = T;
+            p.sweeps = round_sweeps(sw, true, T);
+            p.half = true;
+            break;
+        }
     return p;
 }
 
@@ -1288,43 +1615,70 @@ bool fused_supported(int64_t f, int r) {
 }
 
 hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                        const Workspace &ws, uint32_t *pair_diff, float *out, hipStream_t s) {
+                        const Workspace &ws, uint32_t *pair_diff, float *out, hipStream_t s,
+                        TileUse *use) {
     const bool vec = (d % 4 == 0) && aligned16(g);
     const bool ind = row_of != nullptr;
     const WsPlan plan = ws_plan(f, r, vec, ind);
+    if (use) *use = TileUse{plan.T, plan.half ? 1 : 0};
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind);
+        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind, plan.half);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_WS(TT, SWW)                                                                        \
+#define ASPIS_WS(TT, SWW, HH)                                                                    \
     if (ind)                                                                                     \
-        fused_ws_kernel<TT, 3, SWW, true><<<grid, kWsFill + kWsSelect, lds, s>>>(                \
-            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                  \
+        fused_ws_kernel<TT, 3, SWW, true, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(            \
+            g, row_of, f, d, ws.sel, ws.pos, ws.rows, ws.n_sel, ntiles, pair_diff, out);         \
     else                                                                                         \
-        fused_ws_kernel<TT, 3, SWW, false><<<grid, kWsFill + kWsSelect, lds, s>>>(               \
-            g, nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+        fused_ws_kernel<TT, 3, SWW, false, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(           \
+            g, nullptr, f, d, ws.sel, ws.pos, ws.rows, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_WS_T(TT)                             \
     switch (plan.sweeps) {                         \
-    case 2: ASPIS_WS(TT, 2) break;                 \
-    case 4: ASPIS_WS(TT, 4) break;                 \
-    case 8: ASPIS_WS(TT, 8) break;                 \
-    case 12: ASPIS_WS(TT, 12) break;               \
-    case 16: ASPIS_WS(TT, 16) break;               \
+    case 2: ASPIS_WS(TT, 2, false) break;          \
+    case 4: ASPIS_WS(TT, 4, false) break;          \
+    case 8: ASPIS_WS(TT, 8, false) break;          \
+    case 12: ASPIS_WS(TT, 12, false) break;        \
+    case 16: ASPIS_WS(TT, 16, false) break;        \
     default: return hipErrorInvalidValue;          \
     }
-        switch (T) {
-        case 64: ASPIS_WS_T(64) break;
-        case 32: ASPIS_WS_T(32) break;
-        case 16: ASPIS_WS_T(16) break;
-        case 8: ASPIS_WS_T(8) break;
-        default: return hipErrorInvalidValue;
+#define ASPIS_WS_H(TT)                             \
+    switch (plan.sweeps) {                         \
+    case 16: ASPIS_WS(TT, 16, true) break;         \
+    case 24: ASPIS_WS(TT, 24, true) break;         \
+    case 32: ASPIS_WS(TT, 32, true) break;         \
+    default: return hipErrorInvalidValue;          \
+    }
+        if (plan.half) {
+            switch (T) {
+            case 128:
+                if (plan.sweeps == 8) {
+                    ASPIS_WS(128, 8, true)
+                } else {
+                    ASPIS_WS_H(128)
+                }
+                break;
+            case 64: ASPIS_WS_H(64) break;
+            case 32: ASPIS_WS_H(32) break;
+            case 16: ASPIS_WS_H(16) break;
+            default: return hipErrorInvalidValue;
+            }
+        } else {
+            switch (T) {
+            case 64: ASPIS_WS_T(64) break;
+            case 32: ASPIS_WS_T(32) break;
+            case 16: ASPIS_WS_T(16) break;
+            case 8: ASPIS_WS_T(8) break;
+            default: return hipErrorInvalidValue;
+            }
         }
+#undef ASPIS_WS_H
 #undef ASPIS_WS_T
 #undef ASPIS_WS
         return hipGetLastError();
     }
     const int T = pick_tile(f, f * 4);
+    if (use) *use = TileUse{T, 0};
     if (T == 0) return hipErrorInvalidValue;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)(f * 4 * T + f * 4 + hist_words(T) * 4);

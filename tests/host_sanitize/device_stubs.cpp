@@ -24,14 +24,15 @@ hipError_t launch_select(const int32_t *, const int8_t *, int64_t, int, int, uin
     return hipErrorInvalidValue;
 }
 int pick_median_tile(int64_t f) { return f <= 1000 ? 64 : 0; }
-hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, float *, hipStream_t) {
+hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, float *, hipStream_t,
+                         TileUse *) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_mean(const float *, int64_t, const Workspace &, float *, hipStream_t) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_fused(const float *, const int32_t *, int64_t, int, int64_t, const Workspace &,
-                        uint32_t *, float *, hipStream_t) {
+                        uint32_t *, float *, hipStream_t, TileUse *) {
     return hipErrorInvalidValue;
 }
 bool fused_supported(int64_t, int) { return false; }

@@ -185,6 +185,68 @@ def test_tile_widths(K, r, d):
         _check(g, K, r, q, "median", path)
 
 
+def _ties_case(K: int, q: int, d: int, kind: str, seed: int):
+    """Replicas whose kept values share few distinct high 16-bit halves, so
+    the half-key tiles must read many low halves back: every value 1.0 plus
+    noise in the low 16 bits ("equal_high"), two high halves, signed values
+    with zeros, denormals and NaNs, and constant columns.  Workers 0..q-1
+    return -100 x (a weak attack, detected)."""
+    r = 3
+    rng = np.random.default_rng(seed)
+    f = comb(K, r)
+    low = rng.integers(0, 1 << 16, size=(f, d), dtype=np.uint32)
+    if kind == "equal_high":
+        hi = np.full((f, d), 0x3F80, dtype=np.uint32)
+    elif kind == "two_high":
+        hi = rng.choice(np.array([0x3F80, 0x3F81], dtype=np.uint32), size=(f, d))
+    elif kind == "signed":
+        hi = rng.choice(np.array([0x3F80, 0xBF80, 0x0000, 0x8000, 0x7FC0, 0xFFC0],
+                                 dtype=np.uint32), size=(f, d))
+    else:   # constant
+        hi = np.full((f, d), 0x3F80, dtype=np.uint32)
+        low[:] = 1
+    bits = (hi << np.uint32(16)) | low
+    g = np.repeat(bits.view(np.float32)[:, None, :], r, axis=1).copy()
+    subsets = oracle.assign(K, r)
+    with np.errstate(invalid="ignore"):
+        for i in range(f):
+            for x in range(r):
+                if subsets[i, x] < q:
+                    g[i, x] = np.float32(-100.0) * g[i, x]
+    return g, r
+
+
+@pytest.mark.parametrize("K,q,d,kind", [(11, 2, 132, "equal_high"), (11, 3, 516, "equal_high"),
+                                        (12, 2, 264, "two_high"), (11, 2, 260, "signed"),
+                                        (12, 3, 132, "signed"), (11, 2, 132, "constant"),
+                                        (21, 2, 68, "equal_high"), (26, 3, 36, "two_high")])
+def test_half_key_ties(K, q, d, kind):
+    """The half-key tiles (f >= 128: 165 and 220 files in 128-wide tiles,
+    1330 in 32-wide, 2600 in 16-wide), odd and even kept counts (a third
+    adversary drops one file), ragged last tiles, against the oracle."""
+    g, r = _ties_case(K, q, d, kind, seed=K * 1000 + d)
+    print(f"K={K} q={q} d={d} kind={kind}", flush=True)
+    for path in ("fused", "two_pass"):
+        got, ref = _check(g, K, r, q, "median", path, nan_equal=False)
+        assert got["stats"]["half_keys"] == 1, got["stats"]
+        assert ref["clique"]["success"]
+
+
+_HALF_TILE = {2: 128, 3: 128, 4: 32, 5: 16}
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4, 5])
+@pytest.mark.parametrize("path", ["fused", "two_pass"])
+def test_half_key_tile_widths(idx, path):
+    """The workloads with hundreds of files or more take the half-key tiles
+    at the widths the planner promises (rows of 512, 128 and 64 bytes)."""
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D4[idx])
+    got, _ = _check(g, wl.K, wl.r, wl.q, "median", path)
+    assert got["stats"]["half_keys"] == 1 and got["stats"]["tile_cols"] == _HALF_TILE[idx]
+
+
 def test_guess_from_prefix_is_wrong_then_corrected():
     """The single-pass path guesses the selection from the first 65,536
     coordinates; a worker that deviates only after them makes the guess wrong
