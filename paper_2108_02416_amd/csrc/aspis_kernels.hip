@@ -347,30 +347,34 @@ __device__ __forceinline__ void select_tile(uint32_t *tile, uint32_t *hist, int 
 // (about one row per column on continuous data; every row when all high
 // halves of a column are equal, which costs speed, not exactness).
 //
-// Layout: row j sits in pair-row p = j / 2, in the low (j even) or high
-// (j odd) half of word p*T + (c ^ swz(p % G)).  For an odd row count the
-// high half of the last word is unused and never read.
+// Layout for a streaming role of RPI rows per sweep: rows j and j + RPI,
+// which one lane loads in two consecutive sweeps, share the word of
+// pair-row p = (j / 2RPI) * RPI + j % RPI (j / RPI even: low half), stored
+// at p*T + (c ^ swz(p % G)), so a lane writes whole words.  Rows without a
+// kept value (past the last row, or a dropped file) hold the largest key,
+// 0xFFFF, as do the low halves read back for them: appending elements that
+// are not below any other leaves every rank below the kept count in place.
 
 constexpr int kHalfWindow = 6;                  // key bits per histogram round
 constexpr int kHalfBuckets = 1 << kHalfWindow;
-constexpr int kHalfStride = kHalfBuckets + 4;   // words per column block (16-byte aligned)
+constexpr int kHalfStride = kHalfBuckets + 2;   // words per column block
+constexpr uint32_t kHalfTop = 0xFFFFu;          // largest key: padding rows
 
 __host__ __device__ constexpr int64_t half_hist_words(int T) { return (int64_t)T * kHalfStride; }
+// streaming rows per sweep of a tile T columns wide (threads of four columns)
+__host__ __device__ constexpr int half_rpi(int T) { return 2048 / T; }
+// pair-rows of a tile of `rows` rows: whole pairs of sweeps
+__host__ __device__ constexpr int64_t half_pair_rows(int64_t rows, int T) {
+    return (rows + 2 * half_rpi(T) - 1) / (2 * half_rpi(T)) * half_rpi(T);
+}
 __host__ __device__ constexpr int64_t half_tile_words(int64_t rows, int T) {
-    return (rows + 1) / 2 * T;
+    return half_pair_rows(rows, T) * T;
 }
 
-// Store the high key halves of row j, columns 4cq..4cq+3 (lo2: columns 0,1;
-// hi2: columns 2,3, each column's half in the low 16 bits first).
-template <int T, int G>
-__device__ __forceinline__ void put_half(uint32_t *tile, int j, int cq, uint32_t lo2, uint32_t hi2) {
-    const int p = j >> 1;
-    const int sw = tile_swz<T, G>(p % G);
-    uint16_t *row = reinterpret_cast<uint16_t *>(tile + p * T) + (j & 1);
-    row[2 * ((4 * cq + 0) ^ sw)] = (uint16_t)lo2;
-    row[2 * ((4 * cq + 1) ^ sw)] = (uint16_t)(lo2 >> 16);
-    row[2 * ((4 * cq + 2) ^ sw)] = (uint16_t)hi2;
-    row[2 * ((4 * cq + 3) ^ sw)] = (uint16_t)(hi2 >> 16);
+// Row held by half h of pair-row p.
+template <int RPI>
+__device__ __forceinline__ int half_row(int p, int h) {
+    return (p / RPI) * 2 * RPI + h * RPI + p % RPI;
 }
 
 // The high halves of two full keys, packed (a's in the low 16 bits).
@@ -378,25 +382,46 @@ __device__ __forceinline__ uint32_t pack_high(uint32_t a, uint32_t b) {
     return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-// Lower median of each of the T columns of a half-key tile of n rows
-// (1 <= n <= 65535), by the G lanes stid = c*G + g of column c, written to
-// out[k0 + c] for k0 + c < d.  Row j of the tile is replica row rows[j] of
-// g (rows may point to global memory or LDS).  hist: half_hist_words(T)
-// words, zero on entry and on exit.  The tile is overwritten.
+// Store pair-row p, columns 4cq..4cq+3, from the packed high halves of the
+// even sweep (lo: columns 0,1 and 2,3 in two registers) and of the odd one.
+template <int T, int G>
+__device__ __forceinline__ void put_pairs(uint32_t *tile, int p, int cq, const uint32_t lo[2],
+                                          const uint32_t hi[2]) {
+    uint32_t w[4];
+    w[0] = (lo[0] & 0xFFFFu) | (hi[0] << 16);
+    w[1] = (lo[0] >> 16) | (hi[0] & 0xFFFF0000u);
+    w[2] = (lo[1] & 0xFFFFu) | (hi[1] << 16);
+    w[3] = (lo[1] >> 16) | (hi[1] & 0xFFFF0000u);
+    const int sw = tile_swz<T, G>(p % G);
+    if constexpr (T >= 64 && (32 / G) % 4 == 0) {
+        // the swizzle keeps each aligned group of four columns together
+        *reinterpret_cast<uint4 *>(&tile[p * T + ((4 * cq) ^ sw)]) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tile[p * T + ((4 * cq + e) ^ sw)] = w[e];
+    }
+}
+
+// Lower median of each of the T columns of a half-key tile of np pair-rows
+// holding nk kept values (1 <= nk, 2*np <= 65536), by the G lanes
+// stid = c*G + g of column c, written to out[k0 + c] for k0 + c < d.
+// row(j) gives the replica row of g behind tile row j, or -1 for a padding
+// row.  hist: half_hist_words(T) words, zero on entry and on exit.  The
+// tile is overwritten.
 //
-//  1. one pass for the common magnitude bits and the count of sign-clear
-//     keys (as in select_tile), which settles the sign;
+//  1. one pass: the common magnitude bits of the keys below 0xFFFF, the
+//     count of sign-clear keys and of 0xFFFF keys; settles the sign (or
+//     H = 0xFFFF when the rank falls among those);
 //  2. histogram rounds over the 16-bit keys, each resolving kHalfWindow bits
 //     below the last settled one, until the sought high half H is known
 //     (at most 3 rounds); nothing is compacted, every round reads all keys;
 //  3. one pass collecting the rows whose high half is H into the lane's
 //     16-bit slots (in place), then their low halves are read from g;
 //  4. bitwise radix select on those low halves for the remaining rank.
-template <int T, int G>
-__device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist, int n, int64_t k0,
-                                                 int64_t d, float *out, int stid,
-                                                 const float *__restrict__ g,
-                                                 const int32_t *rows) {
+template <int T, int G, int RPI, typename RowFn>
+__device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist, int np, int nk,
+                                                 int64_t k0, int64_t d, float *out, int stid,
+                                                 const float *__restrict__ g, RowFn &&row) {
     constexpr int STRIDE = G * T;   // words between a lane's pair-rows
     constexpr int BPL = kHalfBuckets / G;
     static_assert(BPL >= 2 && BPL % 2 == 0, "buckets per lane");
@@ -405,16 +430,13 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     uint32_t *base = tile + gl * T + (c ^ tile_swz<T, G>(gl));
     uint16_t *base16 = reinterpret_cast<uint16_t *>(base);
     uint32_t *hcol = hist + c * kHalfStride;
-    const int np = (n + 1) >> 1;
     const int cnt = np > gl ? (np - gl + G - 1) / G : 0;   // words of this lane
-    const bool tail = (n & 1) != 0 && gl == (np - 1) % G;  // its last word holds one row
-    const int full = cnt - (tail ? 1 : 0);
-    uint32_t m = (uint32_t)(n - 1) / 2;
+    uint32_t m = (uint32_t)(nk - 1) / 2;
 
-    // every key of the lane: fn(key, word x, half h) for row 2*(gl + x*G) + h
+    // every key of the lane: fn(key, word x, half h) for pair-row gl + x*G
     auto each = [&](auto &&fn) __attribute__((always_inline)) {
         int x = 0;
-        for (; x + kSelBatch <= full; x += kSelBatch) {
+        for (; x + kSelBatch <= cnt; x += kSelBatch) {
             uint32_t v[kSelBatch];
 #pragma unroll
             for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
@@ -424,81 +446,97 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
                 fn(v[u] >> 16, x + u, 1);
             }
         }
-        for (; x < full; ++x) {
+        for (; x < cnt; ++x) {
             const uint32_t v = base[x * STRIDE];
             fn(v & 0xFFFFu, x, 0);
             fn(v >> 16, x, 1);
         }
-        if (tail) fn(base[full * STRIDE] & 0xFFFFu, full, 0);
     };
     // the lane's x-th 16-bit slot (step 3 on)
     auto slot = [&](int x) __attribute__((always_inline)) -> uint16_t & {
         return base16[(x >> 1) * 2 * STRIDE + (x & 1)];
     };
 
-    // 1. common magnitude bits, keys with the top bit clear (negative values)
-    uint32_t am = 0x7FFFu, om = 0u, z = 0u;
+    // 1. common magnitude bits (keys below 0xFFFF), sign-set and 0xFFFF counts
+    uint32_t am = 0x7FFFu, om = 0u, z = 0u, top = 0u;
     each([&](uint32_t k, int, int) {
+        const bool t = k == kHalfTop;
         const uint32_t mag = (k ^ ((k >> 15) - 1u)) & 0x7FFFu;
-        am &= mag;
-        om |= mag;
+        am &= t ? 0x7FFFu : mag;
+        om |= t ? 0u : mag;
         z += k >> 15;
+        top += t ? 1u : 0u;
     });
     am = group_reduce<G, Op::And>(am);
     om = group_reduce<G, Op::Or>(om);
-    z = (uint32_t)n - group_reduce<G, Op::Add>(z);
+    z = (uint32_t)(2 * np) - group_reduce<G, Op::Add>(z);   // sign-clear keys
+    top = group_reduce<G, Op::Add>(top);
 
-    uint32_t sgn = 0x8000u;
-    if (m < z) sgn = 0u;
-    else m -= z;
-    const uint32_t vm = am ^ om;
     uint32_t H;
-    if (vm == 0u) {   // one magnitude: the sign gives the key
-        H = sgn ? (0x8000u | am) : (~am & 0x7FFFu);
+    uint32_t sgn = 0x8000u;
+    bool settled = false;
+    if (m < z) {
+        sgn = 0u;
     } else {
-        // 2. the keys of the sign lie in [bias, bias + 2^(hb+1)); each round
-        //    splits the window into buckets of 2^sh keys and keeps the one
-        //    holding rank m
-        int hb = 31 - __clz(vm);
-        const uint32_t hi = 0x7FFFu & ~((2u << hb) - 1u);
-        uint32_t bias = sgn ? (0x8000u | (am & hi)) : (~am & hi);
-        for (int round = 0; round < 3; ++round) {
-            const int sh = hb >= kHalfWindow - 1 ? hb - (kHalfWindow - 1) : 0;
-            const uint32_t span = 2u << hb;
-            each([&](uint32_t k, int, int) {
-                const uint32_t o = k - bias;
-                if (o < span) atomicAdd(&hcol[o >> sh], 1u);
-            });
-            uint32_t h[BPL];
-#pragma unroll
-            for (int q = 0; q < BPL; q += 2) {
-                const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[gl * BPL + q]);
-                h[q] = w2.x;
-                h[q + 1] = w2.y;
-            }
-#pragma unroll
-            for (int q = 0; q < BPL; q += 2)
-                *reinterpret_cast<uint2 *>(&hcol[gl * BPL + q]) = make_uint2(0u, 0u);
-            uint32_t tot = 0u;
-#pragma unroll
-            for (int q = 0; q < BPL; ++q) tot += h[q];
-            uint32_t run = group_scan<G>(tot, gl) - tot;
-            uint32_t le = 0u, below = 0u;
-#pragma unroll
-            for (int q = 0; q < BPL; ++q) {
-                run += h[q];
-                const bool ok = run <= m;
-                le += ok ? 1u : 0u;
-                below = ok ? run : below;
-            }
-            le = group_reduce<G, Op::Add>(le);
-            below = group_reduce<G, Op::Max>(below);
-            m -= below;
-            bias += le << sh;
-            if (sh == 0) break;   // 15 bits: windows 14..9, 8..3, 2..0 at most
-            hb = sh - 1;
+        m -= z;
+        const uint32_t below_top = (uint32_t)(2 * np) - z - top;   // sign-set keys below 0xFFFF
+        if (m >= below_top) {
+            H = kHalfTop;
+            m -= below_top;
+            settled = true;
         }
-        H = bias;
+    }
+    if (!settled) {
+        const uint32_t vm = am ^ om;
+        if (vm == 0u) {   // one magnitude: the sign gives the key
+            H = sgn ? (0x8000u | am) : (~am & 0x7FFFu);
+        } else {
+            // 2. the keys of the sign below 0xFFFF lie in [bias, bias +
+            //    2^(hb+1)); each round splits the window into buckets of 2^sh
+            //    keys and keeps the one holding rank m (a 0xFFFF key inside
+            //    the window is counted like any other; one above it is above
+            //    the sought rank)
+            int hb = 31 - __clz(vm);
+            const uint32_t hi = 0x7FFFu & ~((2u << hb) - 1u);
+            uint32_t bias = sgn ? (0x8000u | (am & hi)) : (~am & hi);
+            for (int round = 0; round < 3; ++round) {
+                const int sh = hb >= kHalfWindow - 1 ? hb - (kHalfWindow - 1) : 0;
+                const uint32_t span = 2u << hb;
+                each([&](uint32_t k, int, int) {
+                    const uint32_t o = k - bias;
+                    if (o < span) atomicAdd(&hcol[o >> sh], 1u);
+                });
+                uint32_t h[BPL];
+#pragma unroll
+                for (int q = 0; q < BPL; q += 2) {
+                    const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[gl * BPL + q]);
+                    h[q] = w2.x;
+                    h[q + 1] = w2.y;
+                }
+#pragma unroll
+                for (int q = 0; q < BPL; q += 2)
+                    *reinterpret_cast<uint2 *>(&hcol[gl * BPL + q]) = make_uint2(0u, 0u);
+                uint32_t tot = 0u;
+#pragma unroll
+                for (int q = 0; q < BPL; ++q) tot += h[q];
+                uint32_t run = group_scan<G>(tot, gl) - tot;
+                uint32_t le = 0u, below = 0u;
+#pragma unroll
+                for (int q = 0; q < BPL; ++q) {
+                    run += h[q];
+                    const bool ok = run <= m;
+                    le += ok ? 1u : 0u;
+                    below = ok ? run : below;
+                }
+                le = group_reduce<G, Op::Add>(le);
+                below = group_reduce<G, Op::Max>(below);
+                m -= below;
+                bias += le << sh;
+                if (sh == 0) break;   // 15 bits: windows 14..9, 8..3, 2..0 at most
+                hb = sh - 1;
+            }
+            H = bias;
+        }
     }
 
     // 3. rows whose high half is H, as row numbers in the lane's slots (the
@@ -506,7 +544,7 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     int w = 0;
     each([&](uint32_t k, int x, int h) {
         if (k == H) {
-            slot(w) = (uint16_t)(2 * (gl + x * G) + h);
+            slot(w) = (uint16_t)half_row<RPI>(gl + x * G, h);
             ++w;
         }
     });
@@ -516,13 +554,15 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         uint32_t v[kGather];
 #pragma unroll
         for (int u = 0; u < kGather; ++u) {
-            v[u] = 0u;
-            if (x0 + u < w && valid)
-                v[u] = __float_as_uint(g[(int64_t)rows[slot(x0 + u)] * d + k0 + c]);
+            v[u] = 0xFFFFFFFFu;   // a padding row: the largest key
+            if (x0 + u < w) {
+                const int64_t rr = row(slot(x0 + u));
+                if (rr >= 0 && valid) v[u] = to_key(__float_as_uint(g[rr * d + k0 + c]));
+            }
         }
 #pragma unroll
         for (int u = 0; u < kGather; ++u)
-            if (x0 + u < w) slot(x0 + u) = (uint16_t)(to_key(v[u]) & 0xFFFFu);
+            if (x0 + u < w) slot(x0 + u) = (uint16_t)(v[u] & 0xFFFFu);
     }
 
     // 4. bitwise radix select of rank m among the low halves
@@ -897,14 +937,17 @@ template <int T, int R, int SW, bool IND, bool HALF>
 __global__ void __launch_bounds__(kWsFill + kWsSelect)
 fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
                 const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
-                const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
-                int64_t ntiles, uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
+                const int32_t *__restrict__ n_sel, int64_t ntiles,
+                uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
     extern __shared__ uint32_t smem[];
     constexpr int G = kWsSelect / T;     // selection lanes per column
     constexpr int CPR = T / 4;           // float4 chunks per row segment
     constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
     constexpr int B = ws_batch<R, SW>(); // sweeps per burst of loads
-    constexpr int KW = HALF ? 2 : 4;     // key registers per sweep
+    // key registers per sweep: 4 keys, or (HALF) 4 high halves packed in 2;
+    // a half-key tile's rows are the files themselves
+    constexpr int KW = HALF ? 2 : 4;
+    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T)), "half-key sweeps");
     const int n = *n_sel;
     const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
     uint32_t *hist = smem;               // selection histograms
@@ -927,7 +970,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     if (wave < kWsFill / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
         const int64_t sweep = (int64_t)RPI * R * d;   // elements between sweeps
-        uint32_t keys[SW][KW];   // full keys, or packed high halves (HALF)
+        uint32_t keys[SW][KW];
         // the r replica chunks of one sweep, kept in registers (a value
         // type, so that no per-lane indexing can turn it into memory)
         struct Chunks {
@@ -942,7 +985,8 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
         auto load_sweep = [&](int64_t t, int x) __attribute__((always_inline)) {
             const int64_t col = min(t * T + 4 * cq, d - 4);
             if constexpr (IND) {
-                const int i = j0 + x * RPI < f ? j0 + x * RPI : 0;
+                int i = j0 + x * RPI < f ? j0 + x * RPI : 0;
+                asm volatile("" : "+v"(i));   // row addresses recomputed per tile
                 Chunks c;
 #pragma unroll
                 for (int s = 0; s < R; ++s)
@@ -951,20 +995,27 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
             }
             const float *base = g + (int64_t)j0 * R * d + col;
             int lim = (int)(f - j0);   // sweeps x with x * RPI < lim hold a file
-            // opaque copies of the tile's base address and of the limit:
-            // every row address and check below is recomputed from them,
-            // instead of the compiler carrying one pointer and one lane mask
-            // per sweep across tiles
-            asm volatile("" : "+v"(base), "+v"(lim));
-            const float *rows = (x * RPI < lim) ? base + x * sweep : g + col;
+            // opaque copies of the tile's base address, the limit and the
+            // sweep stride: every row address and check below is recomputed
+            // from them, instead of the compiler carrying one pointer, one
+            // lane mask and one offset per sweep across tiles
+            int64_t stride = sweep;
+            asm volatile("" : "+v"(base), "+v"(lim), "+s"(stride));
+            const float *rows = (x * RPI < lim) ? base + x * stride : g + col;
             Chunks c;
 #pragma unroll
             for (int s = 0; s < R; ++s) c.q[s] = *reinterpret_cast<const uint4 *>(rows + s * d);
             return c;
         };
         // compare the replicas of sweep x and keep the guessed replica's keys
+        // (HALF: its high key halves, packed two to a register, 0xFFFF for a
+        // file past the last or dropped)
         auto proc_sweep = [&](int x, Chunks c) __attribute__((always_inline)) {
             const int i = j0 + x * RPI;   // f <= C(64,3) here
+            if constexpr (HALF) {
+                keys[x][0] = 0xFFFFFFFFu;
+                keys[x][1] = 0xFFFFFFFFu;
+            }
             if (i < f) {
                 uint32_t diff = 0u;
                 int p = 0;
@@ -978,14 +1029,17 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                         ++p;
                     }
                 if (diff) atomicOr(&pd[i], diff);
-                const int s_sel = ps[i] & 7;
+                const int q = ps[i];
+                const int s_sel = q & 7;
                 uint4 w = c.q[0];
 #pragma unroll
                 for (int s = 1; s < R; ++s)
                     if (s_sel == s) w = c.q[s];
                 if constexpr (HALF) {
-                    keys[x][0] = pack_high(to_key(w.x), to_key(w.y));
-                    keys[x][1] = pack_high(to_key(w.z), to_key(w.w));
+                    if (q >= 0) {
+                        keys[x][0] = pack_high(to_key(w.x), to_key(w.y));
+                        keys[x][1] = pack_high(to_key(w.z), to_key(w.w));
+                    }
                 } else {
                     keys[x][0] = to_key(w.x);
                     keys[x][1] = to_key(w.y);
@@ -1015,16 +1069,21 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
             }
         };
         auto put_tile = [&]() __attribute__((always_inline)) {
+            if constexpr (HALF) {
+                // pair-rows j0 + k*RPI of the sweep pairs holding a file
+                int64_t fo = f;   // opaque: compared per tile, not held per pair
+                asm volatile("" : "+s"(fo));
 #pragma unroll
-            for (int x = 0; x < SW; ++x) {
-                const int i = j0 + x * RPI;
-                if (i < f) {
-                    const int q = ps[i];
-                    if (q >= 0) {
-                        if constexpr (HALF)
-                            put_half<T, G>(tile, q >> 3, cq, keys[x][0], keys[x][1]);
-                        else
-                            put_keys<T, G>(tile, q >> 3, cq, keys[x]);
+                for (int k = 0; k < SW / 2; ++k)
+                    if (k * 2 * RPI < fo)
+                        put_pairs<T, G>(tile, j0 + k * RPI, cq, keys[2 * k], keys[2 * k + 1]);
+            } else {
+#pragma unroll
+                for (int x = 0; x < SW; ++x) {
+                    const int i = j0 + x * RPI;
+                    if (i < f) {
+                        const int q = ps[i];
+                        if (q >= 0) put_keys<T, G>(tile, q >> 3, cq, keys[x]);
                     }
                 }
             }
@@ -1051,10 +1110,18 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
             if (n > 0) {
-                if constexpr (HALF)
-                    select_half_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill, g, rows);
-                else
+                if constexpr (HALF) {
+                    // tile row j is file j: its guessed replica's row of g
+                    auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
+                        const int q = j < f ? ps[j] : -1;
+                        if (q < 0) return -1;
+                        return IND ? (int64_t)rt[j * R + (q & 7)] : (int64_t)j * R + (q & 7);
+                    };
+                    select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(f, T), n, t * T, d,
+                                                out, tid - kWsFill, g, row);
+                } else {
                     select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+                }
             }
             __syncthreads();
             __syncthreads();
@@ -1082,7 +1149,9 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
     constexpr int CPR = T / 4;           // float4 chunks per row segment
     constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
     constexpr int B = mws_batch<SW>();   // sweeps per burst of loads
-    constexpr int KW = HALF ? 2 : 4;     // key registers per sweep
+    // key registers per sweep: 4 keys, or (HALF) 4 high halves packed in 2
+    constexpr int KW = HALF ? 2 : 4;
+    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T)), "half-key sweeps");
     const int n = *n_sel;
     if (n <= 0) return;                  // uniform: no workgroup reaches a barrier
     const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
@@ -1097,19 +1166,22 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if (wave < kWsFill / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
-        uint32_t keys[SW][KW];   // full keys, or packed high halves (HALF)
+        uint32_t keys[SW][KW];
         // one 16-byte chunk of kept row j (a lane past the last kept row
         // re-reads row 0, which is never put; past the end of the rows it
         // re-reads the row's last chunk, whose median is never written)
         auto load_row = [&](int64_t t, int x) __attribute__((always_inline)) {
             const int64_t col = min(t * T + 4 * cq, d - 4);
-            const int j = j0 + x * RPI < n ? j0 + x * RPI : 0;
+            int j = j0 + x * RPI < n ? j0 + x * RPI : 0;
+            asm volatile("" : "+v"(j));   // row address recomputed per tile
             return *reinterpret_cast<const uint4 *>(g + (int64_t)rl[j] * d + col);
         };
         auto to_keys = [&](int x, uint4 q) __attribute__((always_inline)) {
             if constexpr (HALF) {
-                keys[x][0] = pack_high(to_key(q.x), to_key(q.y));
-                keys[x][1] = pack_high(to_key(q.z), to_key(q.w));
+                // high key halves; 0xFFFF past the last kept row
+                const bool keep = j0 + x * RPI < n;
+                keys[x][0] = keep ? pack_high(to_key(q.x), to_key(q.y)) : 0xFFFFFFFFu;
+                keys[x][1] = keep ? pack_high(to_key(q.z), to_key(q.w)) : 0xFFFFFFFFu;
             } else {
                 keys[x][0] = to_key(q.x);
                 keys[x][1] = to_key(q.y);
@@ -1134,14 +1206,23 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
             }
         };
         auto put_tile = [&]() __attribute__((always_inline)) {
+            if constexpr (HALF) {
+                int no = n;   // opaque: compared per tile, not held per pair
+                asm volatile("" : "+s"(no));
 #pragma unroll
-            for (int x = 0; x < SW; ++x) {
-                const int j = j0 + x * RPI;
-                if (j < n) {
-                    if constexpr (HALF)
-                        put_half<T, G>(tile, j, cq, keys[x][0], keys[x][1]);
-                    else
-                        put_keys<T, G>(tile, j, cq, keys[x]);
+                for (int k = 0; k < SW / 2; ++k) {
+                    int p = j0 + k * RPI;
+                    // opaque: the LDS addresses are recomputed per tile
+                    // instead of being held in registers for every pair
+                    asm volatile("" : "+v"(p));
+                    if (k * 2 * RPI < no) put_pairs<T, G>(tile, p, cq, keys[2 * k], keys[2 * k + 1]);
+                }
+            } else {
+#pragma unroll
+                for (int x = 0; x < SW; ++x) {
+                    int j = j0 + x * RPI;
+                    asm volatile("" : "+v"(j));   // as above
+                    if (j < n) put_keys<T, G>(tile, j, cq, keys[x]);
                 }
             }
         };
@@ -1164,10 +1245,15 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
     } else {
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if constexpr (HALF)
-                select_half_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill, g, rl);
-            else
+            if constexpr (HALF) {
+                auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
+                    return j < n ? (int64_t)rl[j] : -1;
+                };
+                select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(n, T), n, t * T, d, out,
+                                            tid - kWsFill, g, row);
+            } else {
                 select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+            }
             __syncthreads();
             __syncthreads();
         }
@@ -1443,6 +1529,7 @@ struct WsPlan {
 };
 
 constexpr int64_t kHalfMinRows = 128;
+constexpr int64_t kHalfMaxRows = 60000;   // row numbers (with padding) fit 16 bits
 
 // Sweep counts built for each plan (a sweep past the last row is skipped).
 // Half keys: 8 only for 128 columns, where fewer than 128 rows never take
@@ -1471,7 +1558,7 @@ WsPlan mws_plan(int64_t f, bool vec) {
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         break;
     }
-    if (f >= kHalfMinRows && f < 65535)
+    if (f >= kHalfMinRows && f <= kHalfMaxRows)
         for (int T : {128, 64, 32, 16}) {
             if (T <= p.T) break;
             if (mws_lds_bytes(f, T, true) > kLdsBytes) continue;
@@ -1595,7 +1682,7 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
         p.sweeps = round_sweeps(sw, false, T);
         break;
     }
-    if (f >= kHalfMinRows && f < 65535)
+    if (f >= kHalfMinRows && f <= kHalfMaxRows)
         for (int T : {128, 64, 32, 16}) {
             if (T <= p.T) break;
             if (ws_lds_bytes(f, r, T, ind, true) > kLdsBytes) continue;
@@ -1629,10 +1716,10 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
 #define ASPIS_WS(TT, SWW, HH)                                                                    \
     if (ind)                                                                                     \
         fused_ws_kernel<TT, 3, SWW, true, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(            \
-            g, row_of, f, d, ws.sel, ws.pos, ws.rows, ws.n_sel, ntiles, pair_diff, out);         \
+            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                  \
     else                                                                                         \
         fused_ws_kernel<TT, 3, SWW, false, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(           \
-            g, nullptr, f, d, ws.sel, ws.pos, ws.rows, ws.n_sel, ntiles, pair_diff, out);
+            g, nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_WS_T(TT)                             \
     switch (plan.sweeps) {                         \
     case 2: ASPIS_WS(TT, 2, false) break;          \

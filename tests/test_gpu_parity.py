@@ -189,7 +189,8 @@ def _ties_case(K: int, q: int, d: int, kind: str, seed: int):
     """Replicas whose kept values share few distinct high 16-bit halves, so
     the half-key tiles must read many low halves back: every value 1.0 plus
     noise in the low 16 bits ("equal_high"), two high halves, signed values
-    with zeros, denormals and NaNs, and constant columns.  Workers 0..q-1
+    with zeros, denormals and NaNs (0x7FFF.... NaNs share the largest high
+    half with the tile's padding rows), and constant columns.  Workers 0..q-1
     return -100 x (a weak attack, detected)."""
     r = 3
     rng = np.random.default_rng(seed)
@@ -200,7 +201,7 @@ def _ties_case(K: int, q: int, d: int, kind: str, seed: int):
     elif kind == "two_high":
         hi = rng.choice(np.array([0x3F80, 0x3F81], dtype=np.uint32), size=(f, d))
     elif kind == "signed":
-        hi = rng.choice(np.array([0x3F80, 0xBF80, 0x0000, 0x8000, 0x7FC0, 0xFFC0],
+        hi = rng.choice(np.array([0x3F80, 0xBF80, 0x0000, 0x8000, 0x7FC0, 0xFFC0, 0x7FFF],
                                  dtype=np.uint32), size=(f, d))
     else:   # constant
         hi = np.full((f, d), 0x3F80, dtype=np.uint32)
