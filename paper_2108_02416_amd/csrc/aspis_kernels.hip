@@ -1531,11 +1531,15 @@ struct WsPlan {
 constexpr int64_t kHalfMinRows = 128;
 constexpr int64_t kHalfMaxRows = 60000;   // row numbers (with padding) fit 16 bits
 
-// Sweep counts built for each plan (a sweep past the last row is skipped).
-// Half keys: 8 only for 128 columns, where fewer than 128 rows never take
-// a narrower half-key tile.
+// Sweep counts built for each plan (sweeps past the last row still load,
+// from the first file, so the count is rounded up only a little).  Half
+// keys: an even count; 8 only for 128 columns, where fewer than 128 rows
+// never take a narrower half-key tile, and steps of 2 from 24 to 32 there.
 int round_sweeps(int64_t sw, bool half, int T) {
-    if (half) return sw <= 8 && T == 128 ? 8 : sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
+    if (half) {
+        if (T == 128 && sw > 24) return (int)((sw + 1) / 2 * 2);
+        return sw <= 8 && T == 128 ? 8 : sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
+    }
     return sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
 }
 
@@ -1603,10 +1607,15 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
         if (plan.half) {
             switch (T) {
             case 128:
-                if (plan.sweeps == 8) {
-                    ASPIS_MWS(128, 8, true)
-                } else {
-                    ASPIS_MWS_H(128)
+                switch (plan.sweeps) {
+                case 8: ASPIS_MWS(128, 8, true) break;
+                case 16: ASPIS_MWS(128, 16, true) break;
+                case 24: ASPIS_MWS(128, 24, true) break;
+                case 26: ASPIS_MWS(128, 26, true) break;
+                case 28: ASPIS_MWS(128, 28, true) break;
+                case 30: ASPIS_MWS(128, 30, true) break;
+                case 32: ASPIS_MWS(128, 32, true) break;
+                default: return hipErrorInvalidValue;
                 }
                 break;
             case 64: ASPIS_MWS_H(64) break;
@@ -1739,10 +1748,15 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
         if (plan.half) {
             switch (T) {
             case 128:
-                if (plan.sweeps == 8) {
-                    ASPIS_WS(128, 8, true)
-                } else {
-                    ASPIS_WS_H(128)
+                switch (plan.sweeps) {
+                case 8: ASPIS_WS(128, 8, true) break;
+                case 16: ASPIS_WS(128, 16, true) break;
+                case 24: ASPIS_WS(128, 24, true) break;
+                case 26: ASPIS_WS(128, 26, true) break;
+                case 28: ASPIS_WS(128, 28, true) break;
+                case 30: ASPIS_WS(128, 30, true) break;
+                case 32: ASPIS_WS(128, 32, true) break;
+                default: return hipErrorInvalidValue;
                 }
                 break;
             case 64: ASPIS_WS_H(64) break;
