@@ -226,8 +226,12 @@ def main() -> int:
     red = "mean" if by_mean else "median"
     if last["fused"]:
         alg_bytes = replica_bytes + d * 4.0 + f * 4.0
-        kname = (f"single-pass agreement + {red} kernel (one read): "
-                 + ("fused_mean_kernel" if by_mean else "fused_ws_kernel / fused_kernel"))
+        if by_mean:
+            kname = "fused_mean_kernel"
+        else:
+            kname = (f"fused_ws_kernel, {last['tile_cols']}-column "
+                     + ("half-key" if last["half_keys"] else "full-key") + " tiles")
+        kname = f"single-pass agreement + {red} kernel (one read): {kname}"
     else:
         alg_bytes = replica_bytes + step_out["n_selected"] * d * 4.0 + d * 4.0
         kname = f"agree_kernel + {red}_kernel (two reads)"
@@ -247,8 +251,9 @@ def main() -> int:
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic (seeded Philox, Irwin-Hall N(0,0.01^2) honest gradients, "
-                "ALIE colluders, written on the GPU)",
+        "data": ("synthetic (seeded Philox, written on the GPU): "
+                 + ("Student-t(3)" if wl.dist == synth.DIST_STUDENT3 else "Irwin-Hall N(0,0.01^2)")
+                 + f" honest gradients, {wl.distortion} adversaries"),
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
                    "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
@@ -256,7 +261,8 @@ def main() -> int:
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "path": {"fused": bool(last["fused"]), "speculation_hit": bool(last["speculation_hit"]),
                  "ms_probe": round(last["ms_probe"], 4),
-                 "ms_fallback": round(last["ms_fallback"], 4)},
+                 "ms_fallback": round(last["ms_fallback"], 4),
+                 "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"])},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "parity_on_cpu_sample": parity,
