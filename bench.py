@@ -137,6 +137,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--seed", type=int, default=428)
     ap.add_argument("--two-pass", action="store_true", help="force the two-pass path")
+    ap.add_argument("--alie-z", type=float, default=None,
+                    help="ALIE shift z of the colluders' value mu - z*sigma (default: the "
+                         "workload's, 1.0); z = 0 puts it at the honest mean, next to the median")
     ap.add_argument("--mode", choices=["median", "mean", "paper"], default="median",
                     help="reduction: median (default), mean, or paper (mean when detection "
                          "succeeds, else median)")
@@ -173,6 +176,9 @@ def main() -> int:
     if args.copy_probe:
         return copy_probe(torch, aspis, dev)
     wl = synth.WORKLOADS[args.workload]
+    if args.alie_z is not None:
+        import dataclasses
+        wl = dataclasses.replace(wl, alie_z=args.alie_z)
     K, r, q, d, f = wl.K, wl.r, wl.q, wl.d, wl.f
     subsets = aspis.assign(K, r)
     role, worker, A, D = synth.make_roles(wl, subsets, seed=args.seed)
@@ -257,6 +263,7 @@ def main() -> int:
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
                    "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
+                   **({"alie_z": wl.alie_z} if "alie" in wl.distortion else {}),
                    "replica_bytes": replica_bytes, "parallelism": "single GPU"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "path": {"fused": bool(last["fused"]), "speculation_hit": bool(last["speculation_hit"]),
