@@ -361,14 +361,15 @@ constexpr int kHalfStride = kHalfBuckets + 2;   // words per column block
 constexpr uint32_t kHalfTop = 0xFFFFu;          // largest key: padding rows
 
 __host__ __device__ constexpr int64_t half_hist_words(int T) { return (int64_t)T * kHalfStride; }
-// streaming rows per sweep of a tile T columns wide (threads of four columns)
-__host__ __device__ constexpr int half_rpi(int T) { return 2048 / T; }
+// streaming rows per sweep of a tile T columns wide, for `fill` streaming
+// threads of four columns each
+__host__ __device__ constexpr int half_rpi(int T, int fill) { return fill * 4 / T; }
 // pair-rows of a tile of `rows` rows: whole pairs of sweeps
-__host__ __device__ constexpr int64_t half_pair_rows(int64_t rows, int T) {
-    return (rows + 2 * half_rpi(T) - 1) / (2 * half_rpi(T)) * half_rpi(T);
+__host__ __device__ constexpr int64_t half_pair_rows(int64_t rows, int T, int fill) {
+    return (rows + 2 * half_rpi(T, fill) - 1) / (2 * half_rpi(T, fill)) * half_rpi(T, fill);
 }
-__host__ __device__ constexpr int64_t half_tile_words(int64_t rows, int T) {
-    return half_pair_rows(rows, T) * T;
+__host__ __device__ constexpr int64_t half_tile_words(int64_t rows, int T, int fill) {
+    return half_pair_rows(rows, T, fill) * T;
 }
 
 // Row held by half h of pair-row p.
@@ -925,52 +926,82 @@ fused_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, in
 // between two barriers.  The row loads and the selection overlap inside one
 // workgroup, so a single [f x T] tile of LDS per CU is enough.
 
-constexpr int kWsFill = 512;       // threads of the streaming role
-constexpr int kWsSelect = 512;     // threads of the selection role
+constexpr int kWsThreads = 1024;   // threads of a warp-specialised workgroup
+constexpr int kWsFill = 512;       // threads of the streaming role (default split)
 
 // sweeps per burst of loads: as many as the streaming role's registers hold
 // next to the tile's keys (SW x 4 registers)
 template <int R, int SW>
 constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
 
-template <int T, int R, int SW, bool IND, bool HALF>
-__global__ void __launch_bounds__(kWsFill + kWsSelect)
+template <int T, int R, int SW, bool IND, bool HALF, int FILL>
+__global__ void __launch_bounds__(kWsThreads)
 fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
                 const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
                 const int32_t *__restrict__ n_sel, int64_t ntiles,
                 uint32_t *__restrict__ pair_diff, float *__restrict__ out) {
     extern __shared__ uint32_t smem[];
-    constexpr int G = kWsSelect / T;     // selection lanes per column
+    constexpr int G = (kWsThreads - FILL) / T;   // selection lanes per column
     constexpr int CPR = T / 4;           // float4 chunks per row segment
-    constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
+    constexpr int RPI = FILL / CPR;      // rows per sweep of the streaming role
     constexpr int B = ws_batch<R, SW>(); // sweeps per burst of loads
     // key registers per sweep: 4 keys, or (HALF) 4 high halves packed in 2;
     // a half-key tile's rows are the files themselves
     constexpr int KW = HALF ? 2 : 4;
-    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T)), "half-key sweeps");
+    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T, FILL) && RPI % 8 == 0 && R <= 4),
+                  "half-key sweeps");
     const int n = *n_sel;
     const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
+    const int64_t f8 = (f + 7) / 8;
     uint32_t *hist = smem;               // selection histograms
     uint32_t *tile = smem + hwords;
-    uint32_t *pd = tile + (HALF ? half_tile_words(f, T) : f * T);   // [f] pair-difference bits
-    int32_t *ps = reinterpret_cast<int32_t *>(pd + f);   // [f] (tile row << 3) | slot, or -1
-    int32_t *rt = ps + f;                // [f*R] row table (IND)
+    // per-file words.  Full keys: pd [f] pair-difference bits, ps [f]
+    // (tile row << 3) | slot or -1.  Half keys (tile row = file): one nibble
+    // per file, pd [f/8] pair-difference bits, ps [f/8] 8 | slot or 0
+    uint32_t *pd = tile + (HALF ? half_tile_words(f, T, FILL) : f * T);
+    int32_t *ps = reinterpret_cast<int32_t *>(pd + (HALF ? f8 : f));
+    int32_t *rt = ps + (HALF ? f8 : f);  // [f*R] row table (IND)
     const int tid = threadIdx.x;
-    for (int64_t i = tid; i < f; i += kWsFill + kWsSelect) {
-        pd[i] = 0u;
-        ps[i] = pos[i] >= 0 ? (pos[i] << 3) | sel[i] : -1;
+    if constexpr (HALF) {
+        for (int64_t w = tid; w < f8; w += kWsThreads) {
+            uint32_t v = 0u;
+            for (int e = 0; e < 8; ++e) {
+                const int64_t i = 8 * w + e;
+                if (i < f && pos[i] >= 0) v |= (8u | (uint32_t)sel[i]) << (4 * e);
+            }
+            pd[w] = 0u;
+            ps[w] = (int32_t)v;
+        }
+    } else {
+        for (int64_t i = tid; i < f; i += kWsThreads) {
+            pd[i] = 0u;
+            ps[i] = pos[i] >= 0 ? (pos[i] << 3) | sel[i] : -1;
+        }
     }
+    // the slot nibble of file i (HALF): 8 | slot when kept, else 0
+    auto nib = [&](int i) __attribute__((always_inline)) {
+        return ((uint32_t)ps[i >> 3] >> ((i & 7) * 4)) & 15u;
+    };
     if constexpr (IND)
-        for (int64_t i = tid; i < f * R; i += kWsFill + kWsSelect) rt[i] = row_of[i];
-    for (int i = tid; i < hwords; i += kWsFill + kWsSelect) hist[i] = 0u;
+        for (int64_t i = tid; i < f * R; i += kWsThreads) rt[i] = row_of[i];
+    for (int i = tid; i < hwords; i += kWsThreads) hist[i] = 0u;
     __syncthreads();
-    // roles are whole waves: waves 0-7 stream, waves 8-15 select; every wave
-    // executes the same number of barriers (1 + 2 per tile)
+    // roles are whole waves: the first FILL/64 waves stream, the rest
+    // select; every wave executes the same number of barriers (1 + 2 per
+    // tile)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (wave < kWsFill / 64) {
+    if (wave < FILL / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
         const int64_t sweep = (int64_t)RPI * R * d;   // elements between sweeps
         uint32_t keys[SW][KW];
+        // pair-difference bits of the lane's files (sweep x: bits
+        // NP*(x % PER) of word x / PER), ORed over every tile in registers
+        // and merged into LDS once at the end
+        constexpr int NPB = R * (R - 1) / 2;
+        constexpr int PER = 32 / NPB;
+        uint32_t pdacc[(SW + PER - 1) / PER];
+#pragma unroll
+        for (int a = 0; a < (SW + PER - 1) / PER; ++a) pdacc[a] = 0u;
         // the r replica chunks of one sweep, kept in registers (a value
         // type, so that no per-lane indexing can turn it into memory)
         struct Chunks {
@@ -1028,15 +1059,18 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                         diff |= (y != 0u ? 1u : 0u) << p;
                         ++p;
                     }
-                if (diff) atomicOr(&pd[i], diff);
-                const int q = ps[i];
+                pdacc[x / PER] |= diff << (NPB * (x % PER));
+                // HALF: file i's nibble, word (j0 >> 3) + x*RPI/8 (RPI is a
+                // multiple of 8), shift (j0 & 7) * 4 in every sweep
+                const int w8 = (j0 >> 3) + x * (RPI / 8), sh = (j0 & 7) * 4;
+                const int q = HALF ? (int)(((uint32_t)ps[w8] >> sh) & 15u) : ps[i];
                 const int s_sel = q & 7;
                 uint4 w = c.q[0];
 #pragma unroll
                 for (int s = 1; s < R; ++s)
                     if (s_sel == s) w = c.q[s];
                 if constexpr (HALF) {
-                    if (q >= 0) {
+                    if (q & 8) {
                         keys[x][0] = pack_high(to_key(w.x), to_key(w.y));
                         keys[x][1] = pack_high(to_key(w.z), to_key(w.w));
                     }
@@ -1106,6 +1140,18 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
             if (tn < ntiles) put_tile();
             __syncthreads();
         }
+        // the lane's pair-difference bits into the workgroup's words
+#pragma unroll
+        for (int x = 0; x < SW; ++x) {
+            const int i = j0 + x * RPI;
+            const uint32_t b = (pdacc[x / PER] >> (NPB * (x % PER))) & ((1u << NPB) - 1u);
+            if (i < f && b) {
+                if constexpr (HALF)
+                    atomicOr(&pd[i >> 3], b << ((i & 7) * 4));
+                else
+                    atomicOr(&pd[i], b);
+            }
+        }
     } else {
         __syncthreads();
         for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -1113,22 +1159,25 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                 if constexpr (HALF) {
                     // tile row j is file j: its guessed replica's row of g
                     auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
-                        const int q = j < f ? ps[j] : -1;
-                        if (q < 0) return -1;
+                        const uint32_t q = j < f ? nib(j) : 0u;
+                        if (!(q & 8u)) return -1;
                         return IND ? (int64_t)rt[j * R + (q & 7)] : (int64_t)j * R + (q & 7);
                     };
-                    select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(f, T), n, t * T, d,
-                                                out, tid - kWsFill, g, row);
+                    select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(f, T, FILL), n,
+                                                t * T, d, out, tid - FILL, g, row);
                 } else {
-                    select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+                    select_tile<T, G>(tile, hist, n, t * T, d, out, tid - FILL);
                 }
             }
             __syncthreads();
             __syncthreads();
         }
     }
-    for (int64_t i = tid; i < f; i += kWsFill + kWsSelect)
-        if (pd[i]) atomicOr(&pair_diff[i], pd[i]);
+    __syncthreads();
+    for (int64_t i = tid; i < f; i += kWsThreads) {
+        const uint32_t b = HALF ? ((pd[i >> 3] >> ((i & 7) * 4)) & 15u) : pd[i];
+        if (b) atomicOr(&pair_diff[i], b);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1140,31 +1189,31 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
 template <int SW>
 constexpr int mws_batch() { return SW >= 16 ? 4 : (SW < 6 ? SW : 6); }
 
-template <int T, int SW, bool HALF>
-__global__ void __launch_bounds__(kWsFill + kWsSelect)
+template <int T, int SW, bool HALF, int FILL>
+__global__ void __launch_bounds__(kWsThreads)
 median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
                  const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
     extern __shared__ uint32_t smem[];
-    constexpr int G = kWsSelect / T;     // selection lanes per column
+    constexpr int G = (kWsThreads - FILL) / T;   // selection lanes per column
     constexpr int CPR = T / 4;           // float4 chunks per row segment
-    constexpr int RPI = kWsFill / CPR;   // rows per sweep of the streaming role
+    constexpr int RPI = FILL / CPR;      // rows per sweep of the streaming role
     constexpr int B = mws_batch<SW>();   // sweeps per burst of loads
     // key registers per sweep: 4 keys, or (HALF) 4 high halves packed in 2
     constexpr int KW = HALF ? 2 : 4;
-    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T)), "half-key sweeps");
+    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T, FILL)), "half-key sweeps");
     const int n = *n_sel;
     if (n <= 0) return;                  // uniform: no workgroup reaches a barrier
     const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
     uint32_t *hist = smem;
     uint32_t *tile = smem + hwords;
-    int32_t *rl = reinterpret_cast<int32_t *>(tile + (HALF ? half_tile_words(n, T)
+    int32_t *rl = reinterpret_cast<int32_t *>(tile + (HALF ? half_tile_words(n, T, FILL)
                                                            : (int64_t)n * T));   // [n] kept rows
     const int tid = threadIdx.x;
-    for (int i = tid; i < n; i += kWsFill + kWsSelect) rl[i] = rows[i];
-    for (int i = tid; i < hwords; i += kWsFill + kWsSelect) hist[i] = 0u;
+    for (int i = tid; i < n; i += kWsThreads) rl[i] = rows[i];
+    for (int i = tid; i < hwords; i += kWsThreads) hist[i] = 0u;
     __syncthreads();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (wave < kWsFill / 64) {
+    if (wave < FILL / 64) {
         const int cq = tid % CPR, j0 = tid / CPR;
         uint32_t keys[SW][KW];
         // one 16-byte chunk of kept row j (a lane past the last kept row
@@ -1249,10 +1298,10 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
                 auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
                     return j < n ? (int64_t)rl[j] : -1;
                 };
-                select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(n, T), n, t * T, d, out,
-                                            tid - kWsFill, g, row);
+                select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(n, T, FILL), n, t * T, d,
+                                            out, tid - FILL, g, row);
             } else {
-                select_tile<T, G>(tile, hist, n, t * T, d, out, tid - kWsFill);
+                select_tile<T, G>(tile, hist, n, t * T, d, out, tid - FILL);
             }
             __syncthreads();
             __syncthreads();
@@ -1522,30 +1571,62 @@ hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
 // tile (16..128 columns) with up to 32 sweeps of 2 key registers; taken
 // only when it is wider than the full-key tile, since below kHalfMinRows
 // rows a tile is streamed too quickly to hide the reads of the low halves.
+// Half keys try the even split of streaming and selecting waves first, then
+// 12 streaming waves and 4 selecting ones (kWsFillWide): 1.5x the rows per
+// sweep, so that thousands of rows fit the registers of a 32- or 64-column
+// tile.
 struct WsPlan {
     int T = 0;
     int sweeps = 0;
     bool half = false;
+    int fill = kWsFill;
 };
 
+constexpr int kWsFillWide = 768;
 constexpr int64_t kHalfMinRows = 128;
 constexpr int64_t kHalfMaxRows = 60000;   // row numbers (with padding) fit 16 bits
 
 // Sweep counts built for each plan (sweeps past the last row still load,
 // from the first file, so the count is rounded up only a little).  Half
 // keys: an even count; 8 only for 128 columns, where fewer than 128 rows
-// never take a narrower half-key tile, and steps of 2 from 24 to 32 there.
-int round_sweeps(int64_t sw, bool half, int T) {
+// never take a narrower half-key tile, and steps of 2 from 24 to 32 there;
+// 24 or 32 for the wide split.
+int round_sweeps(int64_t sw, bool half, int T, int fill) {
     if (half) {
+        if (fill == kWsFillWide) return sw <= 24 ? 24 : 32;
         if (T == 128 && sw > 24) return (int)((sw + 1) / 2 * 2);
         return sw <= 8 && T == 128 ? 8 : sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
     }
     return sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
 }
 
+// The half-key plan wider than `narrower` columns, or none; lds(T, fill)
+// gives the kernel's LDS bytes.  The wide split is built for 64 and 32
+// columns only.
+template <typename LdsFn>
+WsPlan half_plan(int64_t f, int narrower, bool allow_wide, LdsFn &&lds) {
+    WsPlan p;
+    if (f < kHalfMinRows || f > kHalfMaxRows) return p;
+    for (int T : {128, 64, 32, 16}) {
+        if (T <= narrower) break;
+        for (int fill : {kWsFill, kWsFillWide}) {
+            if (fill == kWsFillWide && (!allow_wide || T == 128 || T == 16)) continue;
+            const int64_t rpi = half_rpi(T, fill);
+            const int64_t sw = (f + rpi - 1) / rpi;
+            if (sw > 32 || lds(T, fill) > kLdsBytes) continue;
+            p.T = T;
+            p.sweeps = round_sweeps(sw, true, T, fill);
+            p.half = true;
+            p.fill = fill;
+            return p;
+        }
+    }
+    return p;
+}
+
 // LDS of the warp-specialised median: histograms, key tile, row list.
-int64_t mws_lds_bytes(int64_t f, int T, bool half) {
-    return half ? (half_hist_words(T) + half_tile_words(f, T)) * 4 + f * 4
+int64_t mws_lds_bytes(int64_t f, int T, bool half, int fill) {
+    return half ? (half_hist_words(T) + half_tile_words(f, T, fill)) * 4 + f * 4
                 : (hist_words(T) + f * (int64_t)T) * 4 + f * 4;
 }
 
@@ -1553,7 +1634,7 @@ WsPlan mws_plan(int64_t f, bool vec) {
     WsPlan p;
     if (!vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (mws_lds_bytes(f, T, false) > kLdsBytes) continue;
+        if (mws_lds_bytes(f, T, false, kWsFill) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         // 16 sweeps fit the registers only next to the 64-column selection
@@ -1562,19 +1643,10 @@ WsPlan mws_plan(int64_t f, bool vec) {
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         break;
     }
-    if (f >= kHalfMinRows && f <= kHalfMaxRows)
-        for (int T : {128, 64, 32, 16}) {
-            if (T <= p.T) break;
-            if (mws_lds_bytes(f, T, true) > kLdsBytes) continue;
-            const int64_t rpi = kWsFill / (T / 4);
-            const int64_t sw = (f + rpi - 1) / rpi;
-            if (sw > 32) continue;
-            p.T = T;
-            p.sweeps = round_sweeps(sw, true, T);
-            p.half = true;
-            break;
-        }
-    return p;
+    const WsPlan h = half_plan(f, p.T, true, [&](int T, int fill) {
+        return mws_lds_bytes(f, T, true, fill);
+    });
+    return h.T != 0 ? h : p;
 }
 
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
@@ -1585,49 +1657,55 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)mws_lds_bytes(f, T, plan.half);
+        const size_t lds = (size_t)mws_lds_bytes(f, T, plan.half, plan.fill);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_MWS(TT, SWW, HH)                                                               \
-    median_ws_kernel<TT, SWW, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(g, d, ws.rows,      \
-                                                                         ws.n_sel, ntiles, out);
-#define ASPIS_MWS_T(TT)                            \
-    switch (plan.sweeps) {                         \
-    case 4: ASPIS_MWS(TT, 4, false) break;         \
-    case 8: ASPIS_MWS(TT, 8, false) break;         \
-    case 12: ASPIS_MWS(TT, 12, false) break;       \
-    default: return hipErrorInvalidValue;          \
+#define ASPIS_MWS(TT, SWW, HH, FF)                                                           \
+    median_ws_kernel<TT, SWW, HH, FF><<<grid, kWsThreads, lds, s>>>(g, d, ws.rows, ws.n_sel,  \
+                                                                    ntiles, out);
+#define ASPIS_MWS_T(TT)                                  \
+    switch (plan.sweeps) {                               \
+    case 4: ASPIS_MWS(TT, 4, false, kWsFill) break;      \
+    case 8: ASPIS_MWS(TT, 8, false, kWsFill) break;      \
+    case 12: ASPIS_MWS(TT, 12, false, kWsFill) break;    \
+    default: return hipErrorInvalidValue;                \
     }
-#define ASPIS_MWS_H(TT)                            \
-    switch (plan.sweeps) {                         \
-    case 16: ASPIS_MWS(TT, 16, true) break;        \
-    case 24: ASPIS_MWS(TT, 24, true) break;        \
-    case 32: ASPIS_MWS(TT, 32, true) break;        \
-    default: return hipErrorInvalidValue;          \
+#define ASPIS_MWS_H(TT, FF)                              \
+    switch (plan.sweeps) {                               \
+    case 16: ASPIS_MWS(TT, 16, true, FF) break;          \
+    case 24: ASPIS_MWS(TT, 24, true, FF) break;          \
+    case 32: ASPIS_MWS(TT, 32, true, FF) break;          \
+    default: return hipErrorInvalidValue;                \
     }
-        if (plan.half) {
+        if (plan.half && plan.fill == kWsFillWide) {
+            switch (T) {
+            case 64: ASPIS_MWS_H(64, kWsFillWide) break;
+            case 32: ASPIS_MWS_H(32, kWsFillWide) break;
+            default: return hipErrorInvalidValue;
+            }
+        } else if (plan.half) {
             switch (T) {
             case 128:
                 switch (plan.sweeps) {
-                case 8: ASPIS_MWS(128, 8, true) break;
-                case 16: ASPIS_MWS(128, 16, true) break;
-                case 24: ASPIS_MWS(128, 24, true) break;
-                case 26: ASPIS_MWS(128, 26, true) break;
-                case 28: ASPIS_MWS(128, 28, true) break;
-                case 30: ASPIS_MWS(128, 30, true) break;
-                case 32: ASPIS_MWS(128, 32, true) break;
+                case 8: ASPIS_MWS(128, 8, true, kWsFill) break;
+                case 16: ASPIS_MWS(128, 16, true, kWsFill) break;
+                case 24: ASPIS_MWS(128, 24, true, kWsFill) break;
+                case 26: ASPIS_MWS(128, 26, true, kWsFill) break;
+                case 28: ASPIS_MWS(128, 28, true, kWsFill) break;
+                case 30: ASPIS_MWS(128, 30, true, kWsFill) break;
+                case 32: ASPIS_MWS(128, 32, true, kWsFill) break;
                 default: return hipErrorInvalidValue;
                 }
                 break;
-            case 64: ASPIS_MWS_H(64) break;
-            case 32: ASPIS_MWS_H(32) break;
-            case 16: ASPIS_MWS_H(16) break;
+            case 64: ASPIS_MWS_H(64, kWsFill) break;
+            case 32: ASPIS_MWS_H(32, kWsFill) break;
+            case 16: ASPIS_MWS_H(16, kWsFill) break;
             default: return hipErrorInvalidValue;
             }
         } else {
             switch (T) {
             case 64:
                 if (plan.sweeps == 16) {
-                    ASPIS_MWS(64, 16, false)
+                    ASPIS_MWS(64, 16, false, kWsFill)
                 } else {
                     ASPIS_MWS_T(64)
                 }
@@ -1670,40 +1748,31 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
 }
 
 // LDS of the warp-specialised single pass: histograms, key tile, per-file
-// words and, with a row table, the table.
-int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind, bool half) {
-    const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T)
-                               : hist_words(T) + f * (int64_t)T;
-    return words * 4 + f * 8 + (ind ? f * r * 4 : 0);
+// words (half keys: two nibbles per file) and, with a row table, the table.
+int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind, bool half, int fill) {
+    const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T, fill) + 2 * ((f + 7) / 8)
+                               : hist_words(T) + f * (int64_t)T + 2 * f;
+    return words * 4 + (ind ? f * r * 4 : 0);
 }
 
 // Warp-specialised single pass (r = 3, 16-byte aligned rows): plans as for
-// the median above.
+// the median above (the wide split without a row table).
 WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     WsPlan p;
     if (r != 3 || !vec) return p;
     for (int T : {64, 32, 16, 8}) {
-        if (ws_lds_bytes(f, r, T, ind, false) > kLdsBytes) continue;
+        if (ws_lds_bytes(f, r, T, ind, false, kWsFill) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
         const int64_t sw = (f + rpi - 1) / rpi;
         if (sw > 16) continue;
         p.T = T;
-        p.sweeps = round_sweeps(sw, false, T);
+        p.sweeps = round_sweeps(sw, false, T, kWsFill);
         break;
     }
-    if (f >= kHalfMinRows && f <= kHalfMaxRows)
-        for (int T : {128, 64, 32, 16}) {
-            if (T <= p.T) break;
-            if (ws_lds_bytes(f, r, T, ind, true) > kLdsBytes) continue;
-            const int64_t rpi = kWsFill / (T / 4);
-            const int64_t sw = (f + rpi - 1) / rpi;
-            if (sw > 32) continue;
-            p.T = T;
-            p.sweeps = round_sweeps(sw, true, T);
-            p.half = true;
-            break;
-        }
-    return p;
+    const WsPlan h = half_plan(f, p.T, !ind, [&](int T, int fill) {
+        return ws_lds_bytes(f, r, T, ind, true, fill);
+    });
+    return h.T != 0 ? h : p;
 }
 
 bool fused_supported(int64_t f, int r) {
@@ -1720,15 +1789,17 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind, plan.half);
+        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind, plan.half, plan.fill);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_WS(TT, SWW, HH)                                                                    \
-    if (ind)                                                                                     \
-        fused_ws_kernel<TT, 3, SWW, true, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(            \
-            g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);                  \
-    else                                                                                         \
-        fused_ws_kernel<TT, 3, SWW, false, HH><<<grid, kWsFill + kWsSelect, lds, s>>>(           \
-            g, nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+#define ASPIS_WS1(TT, SWW, II, HH, FF)                                                           \
+    fused_ws_kernel<TT, 3, SWW, II, HH, FF><<<grid, kWsThreads, lds, s>>>(                        \
+        g, II ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+#define ASPIS_WS(TT, SWW, HH)                         \
+    if (ind) {                                        \
+        ASPIS_WS1(TT, SWW, true, HH, kWsFill)         \
+    } else {                                          \
+        ASPIS_WS1(TT, SWW, false, HH, kWsFill)        \
+    }
 #define ASPIS_WS_T(TT)                             \
     switch (plan.sweeps) {                         \
     case 2: ASPIS_WS(TT, 2, false) break;          \
@@ -1745,7 +1816,20 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     case 32: ASPIS_WS(TT, 32, true) break;         \
     default: return hipErrorInvalidValue;          \
     }
-        if (plan.half) {
+#define ASPIS_WS_W(TT)                                              \
+    switch (plan.sweeps) {                                          \
+    case 24: ASPIS_WS1(TT, 24, false, true, kWsFillWide) break;     \
+    case 32: ASPIS_WS1(TT, 32, false, true, kWsFillWide) break;     \
+    default: return hipErrorInvalidValue;                           \
+    }
+        if (plan.half && plan.fill == kWsFillWide) {
+            if (ind) return hipErrorInvalidValue;
+            switch (T) {
+            case 64: ASPIS_WS_W(64) break;
+            case 32: ASPIS_WS_W(32) break;
+            default: return hipErrorInvalidValue;
+            }
+        } else if (plan.half) {
             switch (T) {
             case 128:
                 switch (plan.sweeps) {
@@ -1773,9 +1857,11 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
             default: return hipErrorInvalidValue;
             }
         }
+#undef ASPIS_WS_W
 #undef ASPIS_WS_H
 #undef ASPIS_WS_T
 #undef ASPIS_WS
+#undef ASPIS_WS1
         return hipGetLastError();
     }
     const int T = pick_tile(f, f * 4);
