@@ -1602,15 +1602,18 @@ int round_sweeps(int64_t sw, bool half, int T, int fill) {
 
 // The half-key plan wider than `narrower` columns, or none; lds(T, fill)
 // gives the kernel's LDS bytes.  The wide split is built for 64 and 32
-// columns only.
+// columns only.  With a row table (ind) the 128-column tile is not used:
+// the table's loads do not fit the streaming role's registers next to 30
+// sweeps of keys (it spills and loses to the 64-column full-key tile).
 template <typename LdsFn>
-WsPlan half_plan(int64_t f, int narrower, bool allow_wide, LdsFn &&lds) {
+WsPlan half_plan(int64_t f, int narrower, bool ind, LdsFn &&lds) {
     WsPlan p;
     if (f < kHalfMinRows || f > kHalfMaxRows) return p;
     for (int T : {128, 64, 32, 16}) {
         if (T <= narrower) break;
+        if (ind && T == 128) continue;
         for (int fill : {kWsFill, kWsFillWide}) {
-            if (fill == kWsFillWide && (!allow_wide || T == 128 || T == 16)) continue;
+            if (fill == kWsFillWide && (ind || T == 128 || T == 16)) continue;
             const int64_t rpi = half_rpi(T, fill);
             const int64_t sw = (f + rpi - 1) / rpi;
             if (sw > 32 || lds(T, fill) > kLdsBytes) continue;
@@ -1643,7 +1646,7 @@ WsPlan mws_plan(int64_t f, bool vec) {
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         break;
     }
-    const WsPlan h = half_plan(f, p.T, true, [&](int T, int fill) {
+    const WsPlan h = half_plan(f, p.T, false, [&](int T, int fill) {
         return mws_lds_bytes(f, T, true, fill);
     });
     return h.T != 0 ? h : p;
@@ -1769,7 +1772,7 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
         p.sweeps = round_sweeps(sw, false, T, kWsFill);
         break;
     }
-    const WsPlan h = half_plan(f, p.T, !ind, [&](int T, int fill) {
+    const WsPlan h = half_plan(f, p.T, ind, [&](int T, int fill) {
         return ws_lds_bytes(f, r, T, ind, true, fill);
     });
     return h.T != 0 ? h : p;

@@ -60,9 +60,11 @@ def test_workloads_worker_major(idx, flags):
     s = oracle.assign(wl.K, wl.r)
     g, _ = synth.generate(wl, s, d=_D[idx])
     b, _ = _check(g, wl.K, wl.r, wl.q, flags=flags)
-    if flags == 0 and idx in (2, 3):
-        # 455 files: the row table fits next to the 128-column half-key tile
-        assert b["stats"]["tile_cols"] == 128 and b["stats"]["half_keys"] == 1
+    if flags == 0 and idx in (2, 3, 5):
+        # through the row table: 455 files on 64-column full-key tiles, 2,300
+        # on 16-column half-key tiles
+        want = (64, 0) if idx != 5 else (16, 1)
+        assert (b["stats"]["tile_cols"], b["stats"]["half_keys"]) == want
 
 
 @pytest.mark.parametrize("mode", ["mean", "paper"])
