@@ -77,7 +77,15 @@ def cpu_baseline(wl, role, worker, sample_coords: int, gpu_out, gpu_sel, mode: s
         ref = res["out"].astype(np.float64)
         same_out = same_sel and bool(np.all(np.abs(got.astype(np.float64) - ref)
                                             <= 1e-6 * np.maximum(np.abs(ref), 1e-30)))
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                         None)
+    except OSError:
+        pass
     return ({"value": round(value, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+             "cpu_model": model,
              "sample": f"coordinates [0,{sample_coords}) of the same workload "
                        f"({g.nbytes / 1e9:.2f} GB of replicas), {dt:.1f} s single-threaded"},
             same_out)
