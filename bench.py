@@ -30,15 +30,24 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "replica-gradient GB/s through detect+median (K=15,r=3,d=11.2M); % of HBM peak"
-KERNEL_SOURCES = ["paper_2108_02416_amd/csrc/aspis_kernels.hip"]
+KERNEL_SOURCES = ["paper_2108_02416_amd/csrc/aspis_kernels.hip",
+                  "paper_2108_02416_amd/csrc/aspis_internal.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fused_K15_r3_d11.2M.json")
 
 
-def kernel_hash() -> str:
+def kernel_hash(texts=None) -> str:
+    """Hash of the kernel code, comments and whitespace ignored (a comment
+    edit does not invalidate the counters taken on that code)."""
+    import re
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as fh:
-            h.update(fh.read())
+    if texts is None:
+        texts = []
+        for p in KERNEL_SOURCES:
+            with open(os.path.join(ROOT, p), encoding="utf-8") as fh:
+                texts.append(fh.read())
+    for t in texts:
+        t = re.sub(r"//[^\n]*", "", t)
+        h.update(" ".join(t.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -20,9 +20,15 @@
 //                      totalOrder keys, and each column's lower median is
 //                      found by G lanes of one wave (select_tile: one LDS
 //                      histogram round, then a bitwise radix finish).
-//   fused_ws_kernel    agreement + median in one read, warp-specialised: half
-//                      of the waves stream the next tile while the other half
-//                      select on the current one (the headline path, r = 3).
+//   median_ws_kernel   the same median, warp-specialised like the single
+//                      pass (two-pass path, and the rerun after a wrong guess).
+//   fused_ws_kernel    agreement + median in one read, warp-specialised: some
+//                      waves stream the next tile while the others select on
+//                      the current one (the headline path, r = 3).  For
+//                      hundreds of rows or more the LDS tile keeps only the
+//                      high 16 bits of each key (select_half_tile), which
+//                      doubles the tile width; the low halves of the rows
+//                      that tie with the median's high half are read back.
 //   fused_kernel       agreement + median in one read for r = 5, 7 and
 //                      unaligned rows (load, then select, per tile).
 //   fused_mean_kernel  agreement + Case 1 mean in one read.
