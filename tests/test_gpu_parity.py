@@ -167,6 +167,51 @@ def test_random_properties(seed):
     _check(g, K, r, q, "mean", "two_pass", nan_equal=True)
 
 
+def _random_half_case(seed: int):
+    """Random r = 3 replicas at 165 to 2,600 files (the half-key tiles),
+    d a multiple of 4 with a ragged last tile: per file a random partition
+    of the slots into equal replicas, values N(0, 0.01) or on a coarse grid
+    (many ties in the high halves), planted special values and NaNs, and a
+    few workers sending noise on every file."""
+    rng = np.random.default_rng(7000 + seed)
+    K = int(rng.choice([11, 12, 13, 15, 17, 21, 24, 26]))
+    r = 3
+    q = int(rng.integers(0, (K + 1) // 2))
+    d = int(rng.choice([4, 8, 60, 132, 260, 516]))
+    f = comb(K, r)
+    coarse = seed % 3 == 1
+    g = np.empty((f, r, d), dtype=np.float32)
+    for i in range(f):
+        labels = rng.integers(0, rng.integers(1, r + 1), size=r)
+        if coarse:
+            base = (rng.integers(-4, 5, size=(r, d)) * 0.25).astype(np.float32)
+        else:
+            base = (rng.standard_normal((r, d)) * 0.01).astype(np.float32)
+        pick = rng.random((r, d))
+        base[pick < 0.03] = rng.choice(_SPECIAL, size=int((pick < 0.03).sum()))
+        if seed % 2 == 0:
+            base[pick > 0.99] = rng.choice(_NANS, size=int((pick > 0.99).sum()))
+        for x in range(r):
+            g[i, x] = base[labels[x]]
+    if q and seed % 4 == 3:
+        bad = rng.choice(K, size=q, replace=False)
+        subsets = oracle.assign(K, r)
+        for i in range(f):
+            for x in range(r):
+                if subsets[i, x] in bad:
+                    g[i, x] = rng.standard_normal(d).astype(np.float32)
+    return g, K, r, q
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_half_key(seed):
+    g, K, r, q = _random_half_case(seed)
+    print(f"seed={seed} K={K} q={q} d={g.shape[2]}", flush=True)
+    for path in ("fused", "two_pass"):
+        got, _ = _check(g, K, r, q, "median", path)
+        assert got["stats"]["half_keys"] == 1, got["stats"]
+
+
 @pytest.mark.parametrize("K,r,d", [(26, 3, 301), (32, 3, 97), (9, 7, 333), (13, 5, 129),
                                    (26, 3, 300), (32, 3, 96), (29, 3, 200), (9, 7, 332)])
 def test_tile_widths(K, r, d):
