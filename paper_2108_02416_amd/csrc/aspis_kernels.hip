@@ -464,20 +464,37 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         return base16[(x >> 1) * 2 * STRIDE + (x & 1)];
     };
 
-    // 1. common magnitude bits (keys below 0xFFFF), sign-set and 0xFFFF counts
-    uint32_t am = 0x7FFFu, om = 0u, z = 0u, top = 0u;
-    each([&](uint32_t k, int, int) {
-        const bool t = k == kHalfTop;
-        const uint32_t mag = (k ^ ((k >> 15) - 1u)) & 0x7FFFu;
-        am &= t ? 0x7FFFu : mag;
-        om |= t ? 0u : mag;
-        z += k >> 15;
-        top += t ? 1u : 0u;
-    });
-    am = group_reduce<G, Op::And>(am);
-    om = group_reduce<G, Op::Or>(om);
-    z = (uint32_t)(2 * np) - group_reduce<G, Op::Add>(z);   // sign-clear keys
-    top = group_reduce<G, Op::Add>(top);
+    // 1. common magnitude bits (keys below 0xFFFF), sign-set and 0xFFFF
+    //    counts, both keys of a word at once in 16-bit lanes (no carry or
+    //    borrow crosses the halves; counts stay below 2^16)
+    uint32_t am2 = 0x7FFF7FFFu, om2 = 0u, zs2 = 0u, nn2 = 0u;
+    auto stats = [&](uint32_t w) __attribute__((always_inline)) {
+        const uint32_t s2 = w & 0x80008000u;                         // sign-set keys
+        const uint32_t mag2 = (w ^ (0x7FFF7FFFu ^ (s2 - (s2 >> 15)))) & 0x7FFF7FFFu;
+        const uint32_t nt = ~w;                                      // zero: key 0xFFFF
+        const uint32_t nz2 = (((nt & 0x7FFF7FFFu) + 0x7FFF7FFFu) | nt) & 0x80008000u;
+        am2 &= mag2;
+        om2 |= mag2 & (nz2 - (nz2 >> 15));
+        zs2 += s2 >> 15;
+        nn2 += nz2 >> 15;
+    };
+    {
+        int x = 0;
+        for (; x + kSelBatch <= cnt; x += kSelBatch) {
+            uint32_t v[kSelBatch];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u) v[u] = base[(x + u) * STRIDE];
+#pragma unroll
+            for (int u = 0; u < kSelBatch; ++u) stats(v[u]);
+        }
+        for (; x < cnt; ++x) stats(base[x * STRIDE]);
+    }
+    uint32_t am = group_reduce<G, Op::And>(am2 & (am2 >> 16) & 0x7FFFu);
+    uint32_t om = group_reduce<G, Op::Or>((om2 | (om2 >> 16)) & 0x7FFFu);
+    const uint32_t z = (uint32_t)(2 * np) -
+                       group_reduce<G, Op::Add>((zs2 & 0xFFFFu) + (zs2 >> 16));   // sign-clear
+    const uint32_t top = (uint32_t)(2 * np) -
+                         group_reduce<G, Op::Add>((nn2 & 0xFFFFu) + (nn2 >> 16));
 
     uint32_t H;
     uint32_t sgn = 0x8000u;
