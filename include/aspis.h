@@ -25,7 +25,8 @@
  *
  * Asynchrony: aspis_detect and aspis_aggregate only enqueue work on the
  * stream.  aspis_clique is host code.  aspis_detect_aggregate synchronises
- * the stream twice (it needs the agreement graph on the host).
+ * the stream (it needs the agreement graph on the host) and returns with
+ * its work complete.
  *
  * Thread safety: re-entrant; the only global state is the per-thread error
  * message.  Calls that share output buffers must not overlap.
@@ -130,8 +131,9 @@ aspis_status aspis_clique(const uint64_t *disagree_rows, int32_t K, int32_t q,
                           aspis_clique_result *res);
 
 /* Bytes of workspace aspis_aggregate, aspis_detect_aggregate and
- * aspis_detect_aggregate_wm need: four int32 [f] arrays and one int32
- * [f*r] table, each rounded up to 256 bytes, plus 256 bytes of counters.
+ * aspis_detect_aggregate_wm need: three int32 [f] arrays and one int32
+ * [f*r] table, each rounded up to 256 bytes, plus 256 bytes of counters and
+ * 1,024 bytes where the disagreement rows are staged for the host.
  * 0 on invalid arguments. */
 size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d);
 
@@ -184,7 +186,8 @@ typedef struct {
  * with the guess -- the result is exact either way.
  *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
  *   flags   ASPIS_FLAG_* ; stats may be NULL.
- * Synchronises the stream (twice) before returning. */
+ * Synchronises the stream: twice on the single pass (the prefix graph and
+ * the full graph), once more before returning. */
 aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
                                     int32_t q, int64_t d,
                                     const int32_t *subsets_dev,

@@ -257,6 +257,11 @@ size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d) {
 
 namespace {
 
+// Coordinates of the prefix the single pass guesses its selection from
+// (0.3 % of the replica bytes at d = 11.2M).  Any disagreement there is
+// caught; one that starts later only costs the rerun of the reduction.
+constexpr int64_t kProbeCoords = int64_t(1) << 15;
+
 // The worker-major upload of Algorithm 1: worker u returns the gradients of
 // its l = C(K-1,r-1) files in ascending file order, so replica (i,s) is row
 // u*l + k of the upload, where u is slot s's worker and file i is the k-th
@@ -317,7 +322,7 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
     hipStream_t s = static_cast<hipStream_t>(stream);
     aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
     ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success, honest_mask(res),
-                                   row_of, ws, false, sel_out, s));
+                                   row_of, ws, sel_out, nullptr, 0, s));
     if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
     if (mean)
         ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
@@ -382,32 +387,40 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         row_of = ws.row_of;
     }
 
-    const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) &&
+    const bool try_fused = !(flags & ASPIS_FLAG_TWO_PASS) && f <= aspis::kVoteRowsMaxFiles &&
                            (aspis::fused_supported(f, r) || aspis::fused_mean_supported(f, r));
     if (try_fused) {
+        // the detection rows of the last vote, staged in the workspace by
+        // vote_rows_kernel, with stage[64] = "some vote changed"
+        uint64_t staged[65] = {};
+        auto staged_clique = [&](aspis_clique_result *out_res) -> aspis_status {
+            ASPIS_HIP(hipMemcpyAsync(staged, ws.stage, sizeof staged, hipMemcpyDeviceToHost, s));
+            ASPIS_HIP(hipStreamSynchronize(s));
+            return aspis_clique(staged, K, q, out_res);
+        };
         // 1) agreement on a coordinate prefix -> provisional clique and selection
-        const int64_t probe = d < (int64_t(1) << 16) ? d : (int64_t(1) << 16);
+        const int64_t probe = d < kProbeCoords ? d : kProbeCoords;
         local.probe_coords = probe;
         if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
-        ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
-        ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
-        ASPIS_HIP(aspis::launch_agree(grads, row_of, f, r, d, probe, det->pair_diff, s));
-        ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote, det->has_majority,
-                                     det->disagree, s));
+        ASPIS_HIP(aspis::launch_agree_file(grads, row_of, f, r, d, probe, det->pair_diff, s));
+        ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
+                                          det->has_majority, det->disagree, ws.stage, s));
         if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
         aspis_clique_result guess{};
-        if ((st = graph_to_host(&guess)) != ASPIS_OK) { destroy(); return st; }
+        if ((st = staged_clique(&guess)) != ASPIS_OK) { destroy(); return st; }
         // the reduction the guess calls for: the median (Case 2, or MEDIAN
         // mode) or the mean (Case 1 in PAPER mode, or MEAN mode)
         const bool guess_mean = use_mean(mode, &guess);
         if (guess_mean ? aspis::fused_mean_supported(f, r) : aspis::fused_supported(f, r)) {
             local.fused = 1;
             aspis::TileUse fused_tile{};   // stays empty for the mean
+            // the guessed selection; the same launch zeroes pair_diff for
+            // the main pass
             ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, guess.success,
-                                           honest_mask(&guess), row_of, ws, false, nullptr, s));
+                                           honest_mask(&guess), row_of, ws, nullptr,
+                                           det->pair_diff, f, s));
             // 2) one pass: agreement on every coordinate + the reduction with
             //    the guessed selection
-            ASPIS_HIP(aspis::launch_fill_u32(det->pair_diff, f, 0u, s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
             if (guess_mean)
                 ASPIS_HIP(aspis::launch_fused_mean(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
@@ -415,22 +428,21 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s,
                                               &fused_tile));
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
-            ASPIS_HIP(aspis::launch_fill_u64(det->disagree, K, 0ull, s));
-            ASPIS_HIP(aspis::launch_vote(det->pair_diff, subsets_dev, f, r, det->vote,
-                                         det->has_majority, det->disagree, s));
-            if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
-            // 3) the final selection; the guess holds iff it selected the same
-            //    replica of every file and calls for the same reduction
+            ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
+                                              det->has_majority, det->disagree, ws.stage, s));
+            if ((st = staged_clique(res)) != ASPIS_OK) { destroy(); return st; }
+            const bool vote_changed = staged[64] != 0;
+            // 3) the final selection.  The guess selected the same replica of
+            //    every file iff both detections took the same case and
+            //    Case 1 found the same H (the selection depends on H alone),
+            //    or Case 2 voted the same slot for every file (it keeps the
+            //    vote); it holds iff that is so and the reduction is the same
             const int64_t m = kept_files(K, r, f, res);
             if (n_selected) *n_selected = m;
-            ASPIS_HIP(aspis::launch_fill_u32(reinterpret_cast<uint32_t *>(ws.flag), 1, 0u, s));
-            ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
-                                           honest_mask(res), row_of, ws, true, sel_out, s));
-            ASPIS_HIP(aspis::launch_compare_sel(ws.sel, ws.sel2, f, ws.flag, s));
-            int32_t flag = 0;
-            ASPIS_HIP(hipMemcpyAsync(&flag, ws.flag, sizeof flag, hipMemcpyDeviceToHost, s));
-            ASPIS_HIP(hipStreamSynchronize(s));
-            const bool hit = flag == 0 && use_mean(mode, res) == guess_mean;
+            const bool same_sel =
+                guess.success == res->success &&
+                (res->success ? honest_mask(&guess) == honest_mask(res) : !vote_changed);
+            const bool hit = same_sel && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) { destroy(); return fail(ASPIS_ERR_NO_FILES, "selection kept no file"); }
             if (!hit && !use_mean(mode, res) && aspis::pick_median_tile(f) == 0) {
@@ -438,9 +450,14 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
                             (long long)aspis::median_capacity(4));
             }
+            // the workspace describes the final selection from here on (the
+            // rows and positions a rerun of the reduction reads)
+            if (!hit || sel_out)
+                ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
+                                               honest_mask(res), row_of, ws, sel_out, nullptr, 0,
+                                               s));
             if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
             if (!hit) {
-                // ws.pos / ws.rows / ws.n_sel now describe the final selection
                 fused_tile = aspis::TileUse{};
                 if (use_mean(mode, res))
                     ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));

@@ -24,13 +24,12 @@ inline int64_t median_capacity(int T) { return (kLdsBytes - hist_bytes(T)) / (4 
 
 // Workspace layout (byte offsets) for f files.
 struct Workspace {
-    int32_t *sel;    // [f] kept slot or -1
-    int32_t *sel2;   // [f] second selection (to confirm a guessed one)
-    int32_t *pos;    // [f] row of the file in the kept-file list, or -1
-    int32_t *rows;   // [f] kept replica rows (i*r + slot), file order
-    int32_t *n_sel;  // [1] number of kept files
-    int32_t *flag;   // [1] scratch flag
-    int32_t *row_of; // [f*r] row of replica (i,s) in a worker-major upload
+    int32_t *sel;     // [f] kept slot or -1
+    int32_t *pos;     // [f] row of the file in the kept-file list, or -1
+    int32_t *rows;    // [f] kept replica rows (i*r + slot), file order
+    int32_t *n_sel;   // [1] number of kept files
+    uint64_t *stage;  // [65] disagreement rows and a flag, staged for the host
+    int32_t *row_of;  // [f*r] row of replica (i,s) in a worker-major upload
 };
 size_t workspace_bytes(int64_t f, int r);
 Workspace carve_workspace(void *base, int64_t f, int r);
@@ -46,20 +45,33 @@ hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
 hipError_t launch_agree(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         int64_t k_end, uint32_t *pair_diff, hipStream_t s);
 
+// Agreement over coordinates [0, k_end) with one workgroup per file; stores
+// every file's word (no zero fill needed).
+hipError_t launch_agree_file(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                             int64_t k_end, uint32_t *pair_diff, hipStream_t s);
+
 // Per-file vote / majority flag and the disagreement rows (caller zeroes
 // disagree).
 hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets,
                        int64_t f, int r, int8_t *vote, uint8_t *has_majority,
                        uint64_t *disagree, hipStream_t s);
 
-// Selection of Algorithm 1 into the workspace (sel, pos, rows, n_sel).
-// sel is written to ws.sel, or to ws.sel2 when into_sel2 is set, and also
-// to sel_out when it is not NULL.
-// ws.rows lists the kept rows of g (through row_of when it is not NULL).
+// The same in one workgroup (f <= kVoteRowsMaxFiles): writes disagree[0..K)
+// whole, copies the rows to stage[0..K) and sets stage[64] to 1 if a vote
+// changed from the value vote[] held before.
+constexpr int64_t kVoteRowsMaxFiles = 1 << 16;
+hipError_t launch_vote_rows(const uint32_t *pair_diff, const int32_t *subsets, int64_t f,
+                            int r, int K, int8_t *vote, uint8_t *has_majority,
+                            uint64_t *disagree, uint64_t *stage, hipStream_t s);
+
+// Selection of Algorithm 1 into the workspace (sel, pos, rows, n_sel), and
+// into sel_out when it is not NULL.  ws.rows lists the kept rows of g
+// (through row_of when it is not NULL).  zero, when not NULL, receives
+// n_zero zero words in the same launch.
 hipError_t launch_select(const int32_t *subsets, const int8_t *vote,
                          int64_t f, int r, int success, uint64_t honest,
-                         const int32_t *row_of, const Workspace &ws, bool into_sel2,
-                         int32_t *sel_out, hipStream_t s);
+                         const int32_t *row_of, const Workspace &ws,
+                         int32_t *sel_out, uint32_t *zero, int64_t n_zero, hipStream_t s);
 
 // Tile width the median kernel uses for up to f kept files (0: too many).
 int pick_median_tile(int64_t f);
@@ -91,11 +103,6 @@ hipError_t launch_fused_mean(const float *g, const int32_t *row_of, int64_t f, i
                              const Workspace &ws, uint32_t *pair_diff, float *out,
                              hipStream_t s);
 bool fused_mean_supported(int64_t f, int r);
-
-// Host-visible comparison of two selections (writes 1 to *flag if any
-// entry of a and b differ; the caller zeroes flag).
-hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
-                              int32_t *flag, hipStream_t s);
 
 size_t read_probe_sink_words();
 hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink,

@@ -715,8 +715,96 @@ agree_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, in
     }
 }
 
+// Agreement of one file per workgroup over coordinates [0,kend) (the
+// prefix probe of the single pass): the workgroup ORs its lanes' bits and
+// stores the file's word, so pair_diff needs no zero fill and no atomics.
+template <int R, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+agree_file_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
+                  int64_t d, int64_t kend, uint32_t *__restrict__ pair_diff) {
+    __shared__ uint32_t wave_bits[kBlock / 64];
+    constexpr int P = R * (R - 1) / 2;
+    for (int64_t i = blockIdx.x; i < f; i += gridDim.x) {
+        const float *rows[R];
+#pragma unroll
+        for (int s = 0; s < R; ++s) rows[s] = g + replica_row(row_of, i, R, s) * d;
+        uint32_t diff = 0u;
+        for (int64_t k0 = 0; k0 < kend; k0 += kAgreeChunk) {
+            uint32_t v[kAgreeUnroll][R][4];
+#pragma unroll
+            for (int u = 0; u < kAgreeUnroll; ++u) {
+                const int64_t k = k0 + (int64_t)u * kBlock * 4 + (int64_t)threadIdx.x * 4;
+#pragma unroll
+                for (int s = 0; s < R; ++s) {
+                    if (k < kend)
+                        load4<VEC>(rows[s], k, kend, v[u][s]);
+                    else
+                        v[u][s][0] = v[u][s][1] = v[u][s][2] = v[u][s][3] = 0u;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kAgreeUnroll; ++u) {
+                int p = 0;
+#pragma unroll
+                for (int s = 0; s < R; ++s)
+#pragma unroll
+                    for (int t = s + 1; t < R; ++t) {
+                        const uint32_t x = (v[u][s][0] ^ v[u][t][0]) | (v[u][s][1] ^ v[u][t][1]) |
+                                           (v[u][s][2] ^ v[u][t][2]) | (v[u][s][3] ^ v[u][t][3]);
+                        diff |= (x != 0u ? 1u : 0u) << p;
+                        ++p;
+                    }
+            }
+        }
+        uint32_t wdiff = 0u;
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+            if (__ballot((diff >> p) & 1u)) wdiff |= 1u << p;
+        if ((threadIdx.x & 63) == 0) wave_bits[threadIdx.x >> 6] = wdiff;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t b = 0u;
+#pragma unroll
+            for (int w = 0; w < kBlock / 64; ++w) b |= wave_bits[w];
+            pair_diff[i] = b;
+        }
+        __syncthreads();
+    }
+}
+
 // ---------------------------------------------------------------------------
 // vote and disagreement rows
+
+// Eq. (3) for one file from its pair-difference word: the lowest slot of the
+// largest class of bitwise-equal replicas and that class's size.  Calls
+// differ(s, t) for every slot pair whose replicas differ.
+template <typename DiffFn>
+__device__ __forceinline__ void file_vote(uint32_t pd, int r, int *vote_slot, int *class_size,
+                                          DiffFn differ) {
+    // same[s] = bitmask of slots whose replica equals slot s's
+    uint32_t same[8];
+    for (int s = 0; s < r; ++s) same[s] = 1u << s;
+    int p = 0;
+    for (int s = 0; s < r; ++s)
+        for (int t = s + 1; t < r; ++t, ++p) {
+            if (pd >> p & 1u) {
+                differ(s, t);
+            } else {
+                same[s] |= 1u << t;
+                same[t] |= 1u << s;
+            }
+        }
+    int best = 0, best_n = 0;
+    for (int s = 0; s < r; ++s) {
+        const int c = __popc(same[s]);
+        if (c > best_n) {
+            best_n = c;
+            best = s;
+        }
+    }
+    *vote_slot = best;
+    *class_size = best_n;
+}
 
 __global__ void vote_kernel(const uint32_t *__restrict__ pair_diff,
                             const int32_t *__restrict__ subsets, int64_t f,
@@ -725,33 +813,49 @@ __global__ void vote_kernel(const uint32_t *__restrict__ pair_diff,
                             uint64_t *__restrict__ disagree) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < f;
          i += (int64_t)gridDim.x * blockDim.x) {
-        const uint32_t pd = pair_diff[i];
-        // same[s] = bitmask of slots whose replica equals slot s's
-        uint32_t same[8];
-        for (int s = 0; s < r; ++s) same[s] = 1u << s;
-        int p = 0;
-        for (int s = 0; s < r; ++s)
-            for (int t = s + 1; t < r; ++t, ++p) {
-                if (pd >> p & 1u) {
-                    const int us = subsets[i * r + s], ut = subsets[i * r + t];
-                    atomicOr((unsigned long long *)&disagree[us], 1ull << ut);
-                    atomicOr((unsigned long long *)&disagree[ut], 1ull << us);
-                } else {
-                    same[s] |= 1u << t;
-                    same[t] |= 1u << s;
-                }
-            }
         int best = 0, best_n = 0;
-        for (int s = 0; s < r; ++s) {
-            const int c = __popc(same[s]);
-            if (c > best_n) {
-                best_n = c;
-                best = s;
-            }
-        }
+        file_vote(pair_diff[i], r, &best, &best_n, [&](int s, int t) {
+            const int us = subsets[i * r + s], ut = subsets[i * r + t];
+            atomicOr((unsigned long long *)&disagree[us], 1ull << ut);
+            atomicOr((unsigned long long *)&disagree[ut], 1ull << us);
+        });
         vote[i] = (int8_t)best;
         has_majority[i] = (uint8_t)(best_n >= (r + 1) / 2);
     }
+}
+
+// The same in one workgroup, for the single pass (f is at most a few
+// thousand there): the K rows are built in LDS and stored whole (no zero
+// fill), and a copy goes to stage[0..K) for the host, with stage[64] = 1 if
+// any file's vote differs from the one vote[] held before the call.
+__global__ void __launch_bounds__(1024)
+vote_rows_kernel(const uint32_t *__restrict__ pair_diff, const int32_t *__restrict__ subsets,
+                 int64_t f, int r, int K, int8_t *__restrict__ vote,
+                 uint8_t *__restrict__ has_majority, uint64_t *__restrict__ disagree,
+                 uint64_t *__restrict__ stage) {
+    __shared__ unsigned long long rows[64];
+    __shared__ int changed;
+    const int tid = threadIdx.x;
+    if (tid < 64) rows[tid] = 0ull;
+    if (tid == 0) changed = 0;
+    __syncthreads();
+    for (int64_t i = tid; i < f; i += blockDim.x) {
+        int best = 0, best_n = 0;
+        file_vote(pair_diff[i], r, &best, &best_n, [&](int s, int t) {
+            const int us = subsets[i * r + s], ut = subsets[i * r + t];
+            atomicOr(&rows[us], 1ull << ut);
+            atomicOr(&rows[ut], 1ull << us);
+        });
+        if (vote[i] != (int8_t)best) changed = 1;
+        vote[i] = (int8_t)best;
+        has_majority[i] = (uint8_t)(best_n >= (r + 1) / 2);
+    }
+    __syncthreads();
+    if (tid < K) {
+        disagree[tid] = rows[tid];
+        stage[tid] = rows[tid];
+    }
+    if (tid == 0) stage[64] = (uint64_t)changed;
 }
 
 // ---------------------------------------------------------------------------
@@ -762,10 +866,13 @@ select_kernel(const int32_t *__restrict__ subsets,
               const int8_t *__restrict__ vote, int64_t f, int r,
               int success, uint64_t honest, const int32_t *__restrict__ row_of,
               int32_t *__restrict__ sel, int32_t *__restrict__ pos, int32_t *__restrict__ rows,
-              int32_t *__restrict__ n_sel, int32_t *__restrict__ sel_out) {
+              int32_t *__restrict__ n_sel, int32_t *__restrict__ sel_out,
+              uint32_t *__restrict__ zero, int64_t n_zero) {
     __shared__ int wave_tot[16];
     __shared__ int carry;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (zero)
+        for (int64_t i = tid; i < n_zero; i += 1024) zero[i] = 0u;
     if (tid == 0) carry = 0;
     __syncthreads();
     for (int64_t b = 0; b < f; b += 1024) {
@@ -805,13 +912,6 @@ select_kernel(const int32_t *__restrict__ subsets,
         __syncthreads();
     }
     if (tid == 0) *n_sel = carry;
-}
-
-__global__ void compare_sel_kernel(const int32_t *a, const int32_t *b, int64_t f,
-                                   int32_t *flag) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < f;
-         i += (int64_t)gridDim.x * blockDim.x)
-        if (a[i] != b[i]) *flag = 1;
 }
 
 // ---------------------------------------------------------------------------
@@ -1506,9 +1606,13 @@ int64_t tile_grid(int64_t ntiles, size_t lds) {
 // ---------------------------------------------------------------------------
 // launchers
 
+// sel, pos, rows: int32 [f] each; 256 bytes of counters; 1,024 bytes of
+// staged rows; the row table int32 [f*r].  Each part starts 256-aligned.
+constexpr size_t kWsCounters = 256, kWsStage = 1024;
+
 size_t workspace_bytes(int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up((size_t)f * 4) * 4 + 256 + up((size_t)f * r * 4);
+    return up((size_t)f * 4) * 3 + kWsCounters + kWsStage + up((size_t)f * r * 4);
 }
 
 int pick_median_tile(int64_t f) { return pick_tile(f, 0); }
@@ -1519,15 +1623,14 @@ Workspace carve_workspace(void *base, int64_t f, int r) {
     Workspace w;
     w.sel = reinterpret_cast<int32_t *>(p);
     p += up((size_t)f * 4);
-    w.sel2 = reinterpret_cast<int32_t *>(p);
-    p += up((size_t)f * 4);
     w.pos = reinterpret_cast<int32_t *>(p);
     p += up((size_t)f * 4);
     w.rows = reinterpret_cast<int32_t *>(p);
     p += up((size_t)f * 4);
     w.n_sel = reinterpret_cast<int32_t *>(p);
-    w.flag = w.n_sel + 1;
-    p += 256;
+    p += kWsCounters;
+    w.stage = reinterpret_cast<uint64_t *>(p);
+    p += kWsStage;
     w.row_of = reinterpret_cast<int32_t *>(p);
     (void)r;   // the table holds f*r entries (workspace_bytes)
     return w;
@@ -1573,18 +1676,40 @@ hipError_t launch_vote(const uint32_t *pair_diff, const int32_t *subsets, int64_
     return hipGetLastError();
 }
 
-hipError_t launch_select(const int32_t *subsets, const int8_t *vote, int64_t f, int r,
-                         int success, uint64_t honest, const int32_t *row_of, const Workspace &ws,
-                         bool into_sel2, int32_t *sel_out, hipStream_t s) {
-    select_kernel<<<1, 1024, 0, s>>>(subsets, vote, f, r, success, honest, row_of,
-                                     into_sel2 ? ws.sel2 : ws.sel, ws.pos, ws.rows, ws.n_sel,
-                                     sel_out);
+hipError_t launch_vote_rows(const uint32_t *pair_diff, const int32_t *subsets, int64_t f,
+                            int r, int K, int8_t *vote, uint8_t *has_majority,
+                            uint64_t *disagree, uint64_t *stage, hipStream_t s) {
+    if (f > kVoteRowsMaxFiles || K < 1 || K > 64) return hipErrorInvalidValue;
+    vote_rows_kernel<<<1, 1024, 0, s>>>(pair_diff, subsets, f, r, K, vote, has_majority,
+                                        disagree, stage);
     return hipGetLastError();
 }
 
-hipError_t launch_compare_sel(const int32_t *a, const int32_t *b, int64_t f,
-                              int32_t *flag, hipStream_t s) {
-    compare_sel_kernel<<<(unsigned)grid_for((f + 255) / 256, 64), 256, 0, s>>>(a, b, f, flag);
+hipError_t launch_agree_file(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                             int64_t kend, uint32_t *pair_diff, hipStream_t s) {
+    if (f <= 0) return hipSuccess;
+    const unsigned grid = (unsigned)grid_for(f, (int64_t)num_cus() * 8);
+    const bool vec = (d % 4 == 0) && aligned16(g);
+#define ASPIS_AGREE_FILE(RR)                                                                   \
+    if (vec)                                                                                   \
+        agree_file_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, pair_diff); \
+    else                                                                                       \
+        agree_file_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, pair_diff);
+    switch (r) {
+    case 3: ASPIS_AGREE_FILE(3) break;
+    case 5: ASPIS_AGREE_FILE(5) break;
+    case 7: ASPIS_AGREE_FILE(7) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_AGREE_FILE
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const int32_t *subsets, const int8_t *vote, int64_t f, int r,
+                         int success, uint64_t honest, const int32_t *row_of, const Workspace &ws,
+                         int32_t *sel_out, uint32_t *zero, int64_t n_zero, hipStream_t s) {
+    select_kernel<<<1, 1024, 0, s>>>(subsets, vote, f, r, success, honest, row_of, ws.sel,
+                                     ws.pos, ws.rows, ws.n_sel, sel_out, zero, n_zero);
     return hipGetLastError();
 }
 

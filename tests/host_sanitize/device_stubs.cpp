@@ -7,7 +7,7 @@
 
 namespace aspis {
 
-size_t workspace_bytes(int64_t f, int r) { return (size_t)f * 16 + 256 + (size_t)f * r * 4 + 1024; }
+size_t workspace_bytes(int64_t f, int r) { return (size_t)f * 12 + 256 + 1024 + (size_t)f * r * 4 + 1024; }
 Workspace carve_workspace(void *, int64_t, int) { return Workspace{}; }
 hipError_t launch_fill_u32(uint32_t *, int64_t, uint32_t, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_fill_u64(uint64_t *, int64_t, uint64_t, hipStream_t) { return hipErrorInvalidValue; }
@@ -15,12 +15,21 @@ hipError_t launch_agree(const float *, const int32_t *, int64_t, int, int64_t, i
                         hipStream_t) {
     return hipErrorInvalidValue;
 }
+hipError_t launch_agree_file(const float *, const int32_t *, int64_t, int, int64_t, int64_t,
+                             uint32_t *, hipStream_t) {
+    return hipErrorInvalidValue;
+}
 hipError_t launch_vote(const uint32_t *, const int32_t *, int64_t, int, int8_t *, uint8_t *,
                        uint64_t *, hipStream_t) {
     return hipErrorInvalidValue;
 }
+hipError_t launch_vote_rows(const uint32_t *, const int32_t *, int64_t, int, int, int8_t *,
+                            uint8_t *, uint64_t *, uint64_t *, hipStream_t) {
+    return hipErrorInvalidValue;
+}
 hipError_t launch_select(const int32_t *, const int8_t *, int64_t, int, int, uint64_t,
-                         const int32_t *, const Workspace &, bool, int32_t *, hipStream_t) {
+                         const int32_t *, const Workspace &, int32_t *, uint32_t *, int64_t,
+                         hipStream_t) {
     return hipErrorInvalidValue;
 }
 int pick_median_tile(int64_t f) { return f <= 1000 ? 64 : 0; }
@@ -41,9 +50,6 @@ hipError_t launch_fused_mean(const float *, const int32_t *, int64_t, int, int64
     return hipErrorInvalidValue;
 }
 bool fused_mean_supported(int64_t, int) { return false; }
-hipError_t launch_compare_sel(const int32_t *, const int32_t *, int64_t, int32_t *, hipStream_t) {
-    return hipErrorInvalidValue;
-}
 size_t read_probe_sink_words() { return 0; }
 hipError_t launch_read_probe(const void *, size_t, uint32_t *, hipStream_t) {
     return hipErrorInvalidValue;
