@@ -300,9 +300,9 @@ def test_half_key_tile_widths(idx, path):
 
 
 def test_guess_from_prefix_is_wrong_then_corrected():
-    """The single-pass path guesses the selection from the first 65,536
-    coordinates; a worker that deviates only after them makes the guess wrong
-    and the reduction must be redone with the final selection."""
+    """The single-pass path guesses the selection from a prefix of at most
+    65,536 coordinates; a worker that deviates only after it makes the guess
+    wrong and the reduction must be redone with the final selection."""
     wl = synth.WORKLOADS[1]
     s = oracle.assign(wl.K, wl.r)
     d = 65536 + 777
@@ -315,6 +315,57 @@ def test_guess_from_prefix_is_wrong_then_corrected():
     got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused")
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
     assert not ref["clique"]["success"] or ref["clique"]["cliques"][0] != frozenset(range(2, 7))
+
+
+# every flip below lands past the first 65,536 coordinates, beyond any probe
+# prefix of the single pass
+_LATE_D = 65536 + 1028
+
+
+def test_guess_miss_case2_vote_changes():
+    """Detection fails on the prefix and on the whole vector alike, with the
+    same disagreement graph, but one file's vote moves: the guessed Case 2
+    selection keeps the old vote and must be rejected.  Workload 3's file
+    {0,4,5} is not distorted (one adversary) and worker 0 already disagrees
+    with workers 4 and 5 elsewhere; worker 0 deviates in it late."""
+    wl = synth.WORKLOADS[3]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_LATE_D)
+    i = int(np.flatnonzero((s == [0, 4, 5]).all(axis=1))[0])
+    gb = g.view(np.uint32)
+    assert (gb[i, 0] == gb[i, 1]).all() and (gb[i, 1] == gb[i, 2]).all()
+    pre = oracle.detect(np.ascontiguousarray(g[:, :, :65536]), s, wl.K, wl.q)
+    gb[i, 0, _LATE_D - 7] ^= np.uint32(0x40)
+    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused")
+    # the path this test is about: same graph, same failed detection, one
+    # file's vote moved from slot 0 to slot 1
+    assert (pre["disagree"] == ref["disagree"]).all()
+    assert not pre["clique"]["success"] and not ref["clique"]["success"]
+    assert pre["vote"][i] == 0 and ref["vote"][i] == 1
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+
+
+@pytest.mark.parametrize("mode", ["median", "paper"])
+def test_guess_miss_case1_other_clique(mode):
+    """Detection succeeds on the prefix and on the whole vector, with
+    different honest sets: adversary 1 of workload 1 sends honest values on
+    the prefix and its reversed gradients only at the end, so the prefix
+    finds H = {1..6} and the whole vector H = {2..6}.  The Case 1 selection
+    of the guess keeps adversary 1's replicas and must be rejected."""
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = _LATE_D
+    g, _ = synth.generate(wl, s, d=d)
+    for i in range(s.shape[0]):
+        if 1 in s[i]:
+            x = int(np.flatnonzero(s[i] == 1)[0])
+            h = int(np.flatnonzero(s[i] >= 2)[0])   # a slot of an honest worker
+            g[i, x, :d - 64] = g[i, h, :d - 64]
+    pre = oracle.detect(np.ascontiguousarray(g[:, :, :65536]), s, wl.K, wl.q)
+    got, ref = _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    assert pre["clique"]["success"] and pre["clique"]["cliques"][0] == frozenset(range(1, 7))
+    assert ref["clique"]["success"] and ref["clique"]["cliques"][0] == frozenset(range(2, 7))
+    assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
 
 
 def test_guess_holds_on_clean_prefix():
