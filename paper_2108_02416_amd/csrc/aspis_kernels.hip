@@ -419,17 +419,11 @@ __device__ __forceinline__ void put_pairs(uint32_t *tile, int p, int cq, const u
 //  1. one pass: the common magnitude bits of the keys below 0xFFFF, the
 //     count of sign-clear keys and of 0xFFFF keys; settles the sign (or
 //     H = 0xFFFF when the rank falls among those);
-//  2. histogram rounds over the 16-bit keys, each resolving kHalfWindow
-//     bits below the last settled one (at most 3; every round reads all
-//     keys).  As soon as the bucket holding the sought rank has at most
-//     kHalfBuckets keys (usually after the first or second round), one pass
-//     copies those keys with their tile rows into the column's histogram
-//     words and the rounds stop: the candidates are held in registers, a
-//     radix select among them gives H, and only the low halves of the
-//     candidates whose high half is H are read from g and selected the same
-//     way (2a).  Otherwise the rounds continue until H is known, then
-//  3. one pass collects the rows whose high half is H into the lane's
-//     16-bit slots (in place), and their low halves are read from g;
+//  2. histogram rounds over the 16-bit keys, each resolving kHalfWindow bits
+//     below the last settled one, until the sought high half H is known
+//     (at most 3 rounds); nothing is compacted, every round reads all keys;
+//  3. one pass collecting the rows whose high half is H into the lane's
+//     16-bit slots (in place), then their low halves are read from g;
 //  4. bitwise radix select on those low halves for the remaining rank.
 template <int T, int G, int RPI, typename RowFn>
 __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist, int np, int nk,
@@ -505,8 +499,6 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     uint32_t H;
     uint32_t sgn = 0x8000u;
     bool settled = false;
-    uint32_t cb = 0u;      // keys in the bucket of 2a, else 0
-    uint32_t cspan = 0u;   // that bucket's width
     if (m < z) {
         sgn = 0u;
     } else {
@@ -565,105 +557,10 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
                 m -= below;
                 bias += le << sh;
                 if (sh == 0) break;   // 15 bits: windows 14..9, 8..3, 2..0 at most
-                {
-                    uint32_t part = 0u;
-#pragma unroll
-                    for (int q = 0; q < BPL; ++q) part += (uint32_t)(gl * BPL + q) == le ? h[q] : 0u;
-                    const uint32_t n_b = group_reduce<G, Op::Add>(part);
-                    if (n_b <= (uint32_t)kHalfBuckets) {
-                        cb = n_b;
-                        cspan = 1u << sh;
-                        H = bias;   // the bucket's first key; 2a finds H
-                        break;
-                    }
-                }
                 hb = sh - 1;
             }
-            if (cb == 0u) H = bias;
+            H = bias;
         }
-    }
-    const bool valid = k0 + c < d;
-
-    if (cb != 0u) {
-        // 2a. the cb keys of [H, H + cspan) -- the bucket holding rank m
-        //     after the last round -- with their tile rows, into the
-        //     column's histogram words (zero here; word kHalfBuckets counts
-        //     them)
-        const uint32_t span = cspan;
-        uint32_t *cnt_w = hcol + kHalfBuckets;
-        each([&](uint32_t k, int x, int h) {
-            if (k - H < span) {
-                const uint32_t at = atomicAdd(cnt_w, 1u);
-                hcol[at] = k | ((uint32_t)(2 * (gl + x * G) + h) << 16);
-            }
-        });
-        __builtin_amdgcn_wave_barrier();
-        // lane gl holds candidates gl + G*i in registers; bit i of `live`
-        constexpr int NC = kHalfBuckets / G;
-        uint32_t kv[NC];
-        uint32_t live = 0u;
-#pragma unroll
-        for (int i = 0; i < NC; ++i) {
-            const int j = gl + G * i;
-            kv[i] = j < (int)cb ? hcol[j] : 0u;
-            live |= j < (int)cb ? 1u << i : 0u;
-        }
-        // bitwise radix select of rank m among the live 16-bit values
-        // kv[i] & 0xFFFF: split on the highest bit on which they differ,
-        // keep the side holding the rank, until they are all equal; leaves
-        // `live` = the candidates equal to the result and m = the rank
-        // among them
-        auto small_select = [&]() __attribute__((always_inline)) -> uint32_t {
-            uint32_t a = 0xFFFFu, o = 0u;
-            for (int step = 0; step <= 16; ++step) {
-                a = 0xFFFFu;
-                o = 0u;
-#pragma unroll
-                for (int i = 0; i < NC; ++i)
-                    if (live >> i & 1u) {
-                        a &= kv[i];
-                        o |= kv[i];
-                    }
-                a = group_reduce<G, Op::And>(a & 0xFFFFu);
-                o = group_reduce<G, Op::Or>(o & 0xFFFFu);
-                const uint32_t vary = a ^ o;
-                if (vary == 0u) break;
-                const uint32_t bit = 1u << (31 - __clz(vary));
-                uint32_t zc = 0u;
-#pragma unroll
-                for (int i = 0; i < NC; ++i) zc += (live >> i & 1u) && !(kv[i] & bit) ? 1u : 0u;
-                zc = group_reduce<G, Op::Add>(zc);
-                uint32_t want = 0u;
-                if (m >= zc) {
-                    want = bit;
-                    m -= zc;
-                }
-#pragma unroll
-                for (int i = 0; i < NC; ++i)
-                    if ((kv[i] & bit) != want) live &= ~(1u << i);
-            }
-            return a;
-        };
-        H = small_select();
-        // the low halves of the candidates whose high half is H
-#pragma unroll
-        for (int i = 0; i < NC; ++i) {
-            uint32_t key = 0x7FFFFFFFu;   // a padding row: bits of the largest key
-            if (live >> i & 1u) {
-                const uint32_t pr = kv[i] >> 16;
-                const int64_t rr = row(half_row<RPI>((int)(pr >> 1), (int)(pr & 1u)));
-                if (rr >= 0 && valid) key = __float_as_uint(g[rr * d + k0 + c]);
-            }
-            kv[i] = key;
-        }
-#pragma unroll
-        for (int i = 0; i < NC; ++i) kv[i] = to_key(kv[i]) & 0xFFFFu;
-        const uint32_t low = small_select();
-        __builtin_amdgcn_wave_barrier();
-        for (int j = gl; j < (int)cb; j += G) hcol[j] = 0u;
-        if (gl == 0) *cnt_w = 0u;
-        if (gl == 0 && valid) out[k0 + c] = __uint_as_float(from_key((H << 16) | low));
-        return;
     }
 
     // 3. rows whose high half is H, as row numbers in the lane's slots (the
@@ -675,6 +572,7 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
             ++w;
         }
     });
+    const bool valid = k0 + c < d;
     constexpr int kGather = 4;   // row reads in flight per lane
     for (int x0 = 0; x0 < w; x0 += kGather) {
         uint32_t v[kGather];
