@@ -1067,7 +1067,7 @@ constexpr int kWsFill = 512;       // threads of the streaming role (default spl
 template <int R, int SW>
 constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
 
-template <int T, int R, int SW, bool IND, bool HALF, int FILL>
+template <int T, int R, int SW, bool IND, bool HALF, int FILL, bool RTG = false>
 __global__ void __launch_bounds__(kWsThreads)
 fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f, int64_t d,
                 const int32_t *__restrict__ sel, const int32_t *__restrict__ pos,
@@ -1093,7 +1093,10 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     // per file, pd [f/8] pair-difference bits, ps [f/8] 8 | slot or 0
     uint32_t *pd = tile + (HALF ? half_tile_words(f, T, FILL) : f * T);
     int32_t *ps = reinterpret_cast<int32_t *>(pd + (HALF ? f8 : f));
-    int32_t *rt = ps + (HALF ? f8 : f);  // [f*R] row table (IND)
+    // [f*R] row table (IND): staged in LDS, or (RTG) read from global
+    // memory, where it stays cached, when LDS is needed for a wider tile
+    int32_t *rt_lds = ps + (HALF ? f8 : f);
+    const int32_t *rt = RTG ? row_of : rt_lds;
     const int tid = threadIdx.x;
     if constexpr (HALF) {
         for (int64_t w = tid; w < f8; w += kWsThreads) {
@@ -1115,8 +1118,8 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     auto nib = [&](int i) __attribute__((always_inline)) {
         return ((uint32_t)ps[i >> 3] >> ((i & 7) * 4)) & 15u;
     };
-    if constexpr (IND)
-        for (int64_t i = tid; i < f * R; i += kWsThreads) rt[i] = row_of[i];
+    if constexpr (IND && !RTG)
+        for (int64_t i = tid; i < f * R; i += kWsThreads) rt_lds[i] = row_of[i];
     for (int i = tid; i < hwords; i += kWsThreads) hist[i] = 0u;
     __syncthreads();
     // roles are whole waves: the first FILL/64 waves stream, the rest
@@ -1738,6 +1741,7 @@ struct WsPlan {
     int sweeps = 0;
     bool half = false;
     int fill = kWsFill;
+    bool rtg = false;   // row table read from global memory (not in LDS)
 };
 
 constexpr int kWsFillWide = 768;
@@ -1762,16 +1766,18 @@ int round_sweeps(int64_t sw, bool half, int T, int fill) {
 // gives the kernel's LDS bytes.  The wide split is built for 64 and 32
 // columns only.  With a row table (ind) the 128-column tile is not used:
 // the table's loads do not fit the streaming role's registers next to 30
-// sweeps of keys (it spills and loses to the 64-column full-key tile).
+// sweeps of keys (it spills and loses to the 64-column full-key tile).  A
+// row table staged in LDS rules out the wide split; one read from global
+// memory (rtg) does not.
 template <typename LdsFn>
-WsPlan half_plan(int64_t f, int narrower, bool ind, LdsFn &&lds) {
+WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
     WsPlan p;
     if (f < kHalfMinRows || f > kHalfMaxRows) return p;
     for (int T : {128, 64, 32, 16}) {
         if (T <= narrower) break;
         if (ind && T == 128) continue;
         for (int fill : {kWsFill, kWsFillWide}) {
-            if (fill == kWsFillWide && (ind || T == 128 || T == 16)) continue;
+            if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16)) continue;
             const int64_t rpi = half_rpi(T, fill);
             const int64_t sw = (f + rpi - 1) / rpi;
             if (sw > 32 || lds(T, fill) > kLdsBytes) continue;
@@ -1804,7 +1810,7 @@ WsPlan mws_plan(int64_t f, bool vec) {
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         break;
     }
-    const WsPlan h = half_plan(f, p.T, false, [&](int T, int fill) {
+    const WsPlan h = half_plan(f, p.T, false, false, [&](int T, int fill) {
         return mws_lds_bytes(f, T, true, fill);
     });
     return h.T != 0 ? h : p;
@@ -1930,10 +1936,23 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
         p.sweeps = round_sweeps(sw, false, T, kWsFill);
         break;
     }
-    const WsPlan h = half_plan(f, p.T, ind, [&](int T, int fill) {
+    const WsPlan h = half_plan(f, p.T, ind, false, [&](int T, int fill) {
         return ws_lds_bytes(f, r, T, ind, true, fill);
     });
-    return h.T != 0 ? h : p;
+    WsPlan best = h.T != 0 ? h : p;
+    if (ind) {
+        // a wider tile with the wide split when the row table, read from
+        // global memory (where it stays cached), leaves LDS to the keys:
+        // 2,300 files take 32 columns instead of 16
+        WsPlan wide = half_plan(f, best.T, true, true, [&](int T, int fill) {
+            return ws_lds_bytes(f, r, T, false, true, fill);
+        });
+        if (wide.T != 0 && wide.fill == kWsFillWide) {
+            wide.rtg = true;
+            best = wide;
+        }
+    }
+    return best;
 }
 
 bool fused_supported(int64_t f, int r) {
@@ -1950,11 +1969,14 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     if (plan.T != 0) {
         const int T = plan.T;
         const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind, plan.half, plan.fill);
+        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind && !plan.rtg, plan.half, plan.fill);
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
 #define ASPIS_WS1(TT, SWW, II, HH, FF)                                                           \
     fused_ws_kernel<TT, 3, SWW, II, HH, FF><<<grid, kWsThreads, lds, s>>>(                        \
         g, II ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
+#define ASPIS_WS_G(TT, SWW)                                                                      \
+    fused_ws_kernel<TT, 3, SWW, true, true, kWsFillWide, true><<<grid, kWsThreads, lds, s>>>(    \
+        g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_WS(TT, SWW, HH)                         \
     if (ind) {                                        \
         ASPIS_WS1(TT, SWW, true, HH, kWsFill)         \
@@ -1983,8 +2005,16 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     case 32: ASPIS_WS1(TT, 32, false, true, kWsFillWide) break;     \
     default: return hipErrorInvalidValue;                           \
     }
-        if (plan.half && plan.fill == kWsFillWide) {
-            if (ind) return hipErrorInvalidValue;
+        if (plan.half && plan.fill == kWsFillWide && ind) {
+            if (!plan.rtg) return hipErrorInvalidValue;
+            switch (T * 100 + plan.sweeps) {
+            case 6424: ASPIS_WS_G(64, 24) break;
+            case 6432: ASPIS_WS_G(64, 32) break;
+            case 3224: ASPIS_WS_G(32, 24) break;
+            case 3232: ASPIS_WS_G(32, 32) break;
+            default: return hipErrorInvalidValue;
+            }
+        } else if (plan.half && plan.fill == kWsFillWide) {
             switch (T) {
             case 64: ASPIS_WS_W(64) break;
             case 32: ASPIS_WS_W(32) break;
@@ -2018,6 +2048,7 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
             default: return hipErrorInvalidValue;
             }
         }
+#undef ASPIS_WS_G
 #undef ASPIS_WS_W
 #undef ASPIS_WS_H
 #undef ASPIS_WS_T
