@@ -1143,21 +1143,25 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
         struct Chunks {
             uint4 q[R];
         };
-        // issue the row loads of sweep x of tile t.  Every load is in bounds
-        // and unconditional: a lane past the end of the rows (tail tile;
-        // d % 4 == 0) reads the last chunk of its row instead, and a lane
-        // past the last file reads file 0; proc_sweep ignores files past the
-        // last, and a repeated chunk changes neither the agreement bits nor
-        // any written median.
+        // issue the row loads of sweep x of tile t.  Every load is in bounds:
+        // a lane past the end of the rows (tail tile; d % 4 == 0) reads the
+        // last chunk of its row instead (a repeated chunk changes neither
+        // the agreement bits nor any written median), and a lane past the
+        // last file loads nothing (proc_sweep ignores it).
         auto load_sweep = [&](int64_t t, int x) __attribute__((always_inline)) {
             const int64_t col = min(t * T + 4 * cq, d - 4);
             if constexpr (IND) {
-                int i = j0 + x * RPI < f ? j0 + x * RPI : 0;
+                int i = j0 + x * RPI;
                 asm volatile("" : "+v"(i));   // row addresses recomputed per tile
                 Chunks c;
+                if (i < f) {
 #pragma unroll
-                for (int s = 0; s < R; ++s)
-                    c.q[s] = load_stream(g + (int64_t)rt[i * R + s] * d + col);
+                    for (int s = 0; s < R; ++s)
+                        c.q[s] = load_stream(g + (int64_t)rt[i * R + s] * d + col);
+                } else {
+#pragma unroll
+                    for (int s = 0; s < R; ++s) c.q[s] = make_uint4(0u, 0u, 0u, 0u);
+                }
                 return c;
             }
             const float *base = g + (int64_t)j0 * R * d + col;
@@ -1168,10 +1172,15 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
             // lane mask and one offset per sweep across tiles
             int64_t stride = sweep;
             asm volatile("" : "+v"(base), "+v"(lim), "+s"(stride));
-            const float *rows = (x * RPI < lim) ? base + x * stride : g + col;
             Chunks c;
+            if (x * RPI < lim) {
+                const float *rows = base + x * stride;
 #pragma unroll
-            for (int s = 0; s < R; ++s) c.q[s] = load_stream(rows + s * d);
+                for (int s = 0; s < R; ++s) c.q[s] = load_stream(rows + s * d);
+            } else {
+#pragma unroll
+                for (int s = 0; s < R; ++s) c.q[s] = make_uint4(0u, 0u, 0u, 0u);
+            }
             return c;
         };
         // compare the replicas of sweep x and keep the guessed replica's keys
