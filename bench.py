@@ -13,8 +13,9 @@ ALIE adversaries; 61.15 GB of replicas.  Inputs are synthetic and seeded
 Prints ONE JSON line.  `value` is replica-gradient GB/s (f*r*d*4 bytes per
 step / step time).  `roofline` reports the dominant kernel (the single-pass
 agreement + median kernel) from HIP events recorded on its stream inside the
-library; `cpu_baseline` times the oracle on a bounded coordinate sample of
-the same workload on the host.
+library; `read_ceiling` is a linear read of the same tensor with the same
+loads (the part's ceiling for this allocation); `cpu_baseline` times the
+oracle on a bounded coordinate sample of the same workload on the host.
 """
 from __future__ import annotations
 
@@ -100,6 +101,27 @@ def cpu_baseline(wl, role, worker, sample_coords: int, gpu_out, gpu_sel, mode: s
             same_out)
 
 
+def read_ceiling(torch, aspis, grads, reps: int = 5) -> dict:
+    """A linear read of the replica tensor itself (aspis_read_probe: the
+    same non-temporal 16-byte loads as the single pass), timed with HIP
+    events on the current stream: the bandwidth ceiling of the part for
+    this allocation.  Median of `reps` reads after two warm-ups."""
+    sink = aspis.read_probe(grads)
+    for _ in range(2):
+        aspis.read_probe(grads, sink)
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        aspis.read_probe(grads, sink)
+        b.record()
+        b.synchronize()
+        ts.append(a.elapsed_time(b))
+    ms = sorted(ts)[reps // 2]
+    nbytes = grads.numel() * grads.element_size() // 16 * 16
+    return {"ms": round(ms, 4), "GB/s": round(nbytes / (ms / 1e3) / 1e9, 1), "bytes": nbytes}
+
+
 def copy_probe(torch, aspis, dev, nbytes: int = 1 << 32) -> int:
     """Kernels of known traffic for scaling the FETCH_SIZE / WRITE_SIZE
     counters: an elementwise negation (reads and writes nbytes) and the
@@ -163,6 +185,8 @@ def main() -> int:
     ap.add_argument("--layout", choices=["file", "worker"], default="file",
                     help="replicas as one [f][r][d] tensor (file) or as the workers' uploads "
                          "[K][l][d] (worker, aspis_detect_aggregate_wm)")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the linear read of the replica tensor after the timed steps")
     ap.add_argument("--cpu-sample", type=int, default=1 << 20,
                     help="coordinates of the oracle's CPU-baseline sample (0 = skip)")
     ap.add_argument("--simulate", action="store_true",
@@ -264,6 +288,12 @@ def main() -> int:
                 "traffic": measured_traffic(alg_bytes), "kernel": kname,
                 "kernel_ms": round(ms_kernel, 4), "algorithmic_bytes": alg_bytes}
 
+    ceiling = None
+    if not args.no_ceiling:
+        ceiling = read_ceiling(torch, aspis, grads)
+        ceiling["kernel_frac"] = round(achieved / ceiling["GB/s"], 4)
+        ceiling["step_frac"] = round(value / ceiling["GB/s"], 4)
+
     cpu = None
     parity = None
     if args.cpu_sample > 0:
@@ -288,6 +318,7 @@ def main() -> int:
                  "ms_fallback": round(last["ms_fallback"], 4),
                  "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"])},
         "roofline": roofline,
+        "read_ceiling": ceiling,
         "cpu_baseline": cpu,
         "parity_on_cpu_sample": parity,
     }
