@@ -257,10 +257,15 @@ size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d) {
 
 namespace {
 
-// Coordinates of the prefix the single pass guesses its selection from
-// (0.3 % of the replica bytes at d = 11.2M).  Any disagreement there is
+// Coordinates of the prefix the single pass guesses its selection from:
+// about 2^24 replica words (200 MB; 0.3 % of the bytes at f = 455, d =
+// 11.2M), between 4,096 and 32,768 coordinates.  Any disagreement there is
 // caught; one that starts later only costs the rerun of the reduction.
-constexpr int64_t kProbeCoords = int64_t(1) << 15;
+int64_t probe_coords(int64_t f, int64_t d) {
+    int64_t p = (int64_t(1) << 24) / (f > 0 ? f : 1);
+    p = p < 4096 ? 4096 : p > 32768 ? 32768 : p;
+    return d < p ? d : p;
+}
 
 // The worker-major upload of Algorithm 1: worker u returns the gradients of
 // its l = C(K-1,r-1) files in ascending file order, so replica (i,s) is row
@@ -399,7 +404,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             return aspis_clique(staged, K, q, out_res);
         };
         // 1) agreement on a coordinate prefix -> provisional clique and selection
-        const int64_t probe = d < kProbeCoords ? d : kProbeCoords;
+        const int64_t probe = probe_coords(f, d);
         local.probe_coords = probe;
         if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
         ASPIS_HIP(aspis::launch_agree_file(grads, row_of, f, r, d, probe, det->pair_diff, s));
