@@ -721,7 +721,11 @@ agree_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, in
 #pragma unroll
         for (int p = 0; p < P; ++p)
             if (__ballot((diff >> p) & 1u)) wdiff |= 1u << p;
-        if ((threadIdx.x & 63) == 0 && wdiff) atomicOr(&pair_diff[i], wdiff);
+        // the word already holds the bits after the first chunks of a file
+        // that differs: read it first, so that the other chunks' waves of
+        // that file do not all queue atomics on one address
+        if ((threadIdx.x & 63) == 0 && wdiff && (wdiff & ~__atomic_load_n(&pair_diff[i], __ATOMIC_RELAXED)))
+            atomicOr(&pair_diff[i], wdiff);
     }
 }
 
