@@ -10,9 +10,13 @@
 //
 //   agree_kernel       Eq. (4): per file, OR over coordinates of "slot pair p
 //                      differs"; one coalesced stream over the r rows.
+//   agree_file_kernel  the same over a coordinate prefix, one workgroup per
+//                      file (the probe of the single pass).
 //   vote_kernel        Eq. (3) majority per file and the K x K disagreement
 //                      rows (Section 4: edge iff the pair agrees on all
 //                      common files).
+//   vote_rows_kernel   the same in one workgroup, rows built in LDS and
+//                      staged for the host (the single pass).
 //   select_kernel      Algorithm 1 selection (Case 1 honest replica / Case 2
 //                      majority) and the ordered list of kept rows.
 //   median_kernel      Algorithm 1 Case 2 coordinate-wise median: a tile of T
