@@ -1781,18 +1781,17 @@ int round_sweeps(int64_t sw, bool half, int T, int fill) {
 
 // The half-key plan wider than `narrower` columns, or none; lds(T, fill)
 // gives the kernel's LDS bytes.  The wide split is built for 64 and 32
-// columns only.  With a row table (ind) the 128-column tile is not used:
-// the table's loads do not fit the streaming role's registers next to 30
-// sweeps of keys (it spills and loses to the 64-column full-key tile).  A
-// row table staged in LDS rules out the wide split; one read from global
-// memory (rtg) does not.
+// columns only.  With a row table (ind) the 128-column tile spills 15
+// registers of the streaming role next to 30 sweeps of keys, and still
+// beats the 64-column full-key tile (10.9 against 11.6 ms at 455 files,
+// d = 11.2M, one process and allocation).  A row table staged in LDS rules
+// out the wide split; one read from global memory (rtg) does not.
 template <typename LdsFn>
 WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
     WsPlan p;
     if (f < kHalfMinRows || f > kHalfMaxRows) return p;
     for (int T : {128, 64, 32, 16}) {
         if (T <= narrower) break;
-        if (ind && T == 128) continue;
         for (int fill : {kWsFill, kWsFillWide}) {
             if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16)) continue;
             const int64_t rpi = half_rpi(T, fill);

@@ -61,10 +61,10 @@ def test_workloads_worker_major(idx, flags):
     g, _ = synth.generate(wl, s, d=_D[idx])
     b, _ = _check(g, wl.K, wl.r, wl.q, flags=flags)
     if flags == 0 and idx in (2, 3, 5):
-        # through the row table: 455 files on 64-column full-key tiles, 2,300
-        # on 32-column half-key tiles (the table read from global memory, so
-        # that the wide split's tile fits LDS)
-        want = (64, 0) if idx != 5 else (32, 1)
+        # through the row table: 455 files on 128-column half-key tiles,
+        # 2,300 on 32-column ones (the table read from global memory, so that
+        # the wide split's tile fits LDS)
+        want = (128, 1) if idx != 5 else (32, 1)
         assert (b["stats"]["tile_cols"], b["stats"]["half_keys"]) == want
 
 
