@@ -143,6 +143,11 @@ def test_worker_major_entry_validates_before_touching_the_gpu():
     assert call(None, 7, 3, 2, 10) == aspis.ERR_INVALID_ARG      # NULL replicas
     assert call(16, 7, 3, 2, 10, ws_bytes=64) == aspis.ERR_BUFFER_SMALL
     assert call(16, 7, 3, 2, 10, ws=257) == aspis.ERR_INVALID_ARG  # unaligned workspace
-    # the workspace covers the f*r row table of the worker-major layout
-    f, r = 35, 3
-    assert L.aspis_aggregate_workspace(7, 3, 10) >= 4 * f * 4 + f * r * 4
+    # the workspace of include/aspis.h: three int32 [f] arrays and the f*r
+    # row table of the worker-major layout, each rounded up to 256 bytes,
+    # 256 bytes of counters and 1,024 of staged detection rows
+    def up(x):
+        return (x + 255) // 256 * 256
+    for K, r in ((7, 3), (15, 3), (25, 3), (9, 5), (9, 7)):
+        f = comb(K, r)
+        assert L.aspis_aggregate_workspace(K, r, 10) == 3 * up(4 * f) + 256 + 1024 + up(4 * f * r)
