@@ -186,6 +186,9 @@ typedef struct {
  * with the guess -- the result is exact either way.
  *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
  *   flags   ASPIS_FLAG_* ; stats may be NULL.
+ * Errors as aspis_aggregate's, except that on NO_FILES `out` holds no
+ * result rather than being untouched: the single pass may have written it
+ * with the guessed selection before the final one kept no file.
  * Synchronises the stream: twice on the single pass (the prefix graph and
  * the full graph), once more before returning. */
 aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
