@@ -151,3 +151,13 @@ def test_worker_major_entry_validates_before_touching_the_gpu():
     for K, r in ((7, 3), (15, 3), (25, 3), (9, 5), (9, 7)):
         f = comb(K, r)
         assert L.aspis_aggregate_workspace(K, r, 10) == 3 * up(4 * f) + 256 + 1024 + up(4 * f * r)
+
+
+def test_read_probe_validates_before_touching_the_gpu():
+    L = aspis.lib()
+    sink = 256   # never dereferenced: every call below is refused first
+    assert L.aspis_read_probe(None, 64, sink, None) == aspis.ERR_INVALID_ARG
+    assert L.aspis_read_probe(4096, 64, None, None) == aspis.ERR_INVALID_ARG
+    assert L.aspis_read_probe(4096, 40, sink, None) == aspis.ERR_INVALID_ARG   # not 16-byte chunks
+    assert L.aspis_read_probe(4100, 64, sink, None) == aspis.ERR_INVALID_ARG   # unaligned
+    assert L.aspis_read_probe_sink_words() > 0

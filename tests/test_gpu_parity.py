@@ -415,3 +415,18 @@ def test_unaligned_rows_use_scalar_loads():
     gd.copy_(torch.from_numpy(g))
     got = aspis.detect_aggregate(gd, wl.K, wl.r, wl.q)
     assert_same_floats(to_np(got["out"]), ref["out"])
+
+
+@pytest.mark.parametrize("nbytes", [16, 48 * 1024 + 16, (3 << 20) + 48])
+def test_read_probe_reads_every_chunk_once(nbytes):
+    """The read-bandwidth probe: the XOR of its per-thread checksum words is
+    the XOR of every 32-bit word of the buffer (each 16-byte chunk read
+    exactly once, ragged tail included)."""
+    import torch
+    rng = np.random.default_rng(nbytes)
+    words = rng.integers(0, 2**32, size=nbytes // 4, dtype=np.uint64).astype(np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).to(device())
+    sink = aspis.read_probe(buf)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(to_np(sink).view(np.uint32))
+    assert got == np.bitwise_xor.reduce(words)
