@@ -119,6 +119,26 @@ def test_many_files_paper_mode():
     assert e.value.status == aspis.ERR_INVALID_ARG
 
 
+def test_largest_K_bit_63():
+    """K = 64, the largest the device entry points take: f = C(64,3) = 41,664
+    files, adversaries 0, 31 and 63 (the ends of both 32-bit halves of a
+    disagreement row), reversed gradients.  Detection succeeds with H = the
+    other 61 workers; the mean (PAPER mode) runs on the two-pass path."""
+    K, r, q, d = 64, 3, 3, 24
+    s = oracle.assign(K, r)
+    f = s.shape[0]
+    rng = np.random.default_rng(64)
+    true = (0.01 * rng.standard_normal((f, d))).astype(np.float32)
+    g = np.repeat(true[:, None, :], r, axis=1)
+    for a in (0, 31, 63):
+        fi, sl = np.nonzero(s == a)
+        g[fi, sl] = -100.0 * true[fi]
+    got, ref = _check(g, K, r, q, "paper", "fused")
+    assert ref["clique"]["success"]
+    assert ref["clique"]["cliques"][0] == frozenset(range(K)) - {0, 31, 63}
+    assert got["stats"]["fused"] == 0   # too many files for the single pass
+
+
 _SPECIAL = np.array([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 3.4e38, -3.4e38],
                     dtype=np.float32)
 _NANS = np.array([0x7FC00000, 0x7FC00001, 0xFFC00000, 0x7F800001, 0xFFFFFFFF],
