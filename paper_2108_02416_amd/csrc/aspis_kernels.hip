@@ -1765,15 +1765,24 @@ constexpr int kWsFillWide = 768;
 constexpr int64_t kHalfMinRows = 128;
 constexpr int64_t kHalfMaxRows = 60000;   // row numbers (with padding) fit 16 bits
 
-// Sweep counts built for each plan (sweeps past the last row still load,
-// from the first file, so the count is rounded up only a little).  Half
-// keys: an even count; 8 only for 128 columns, where fewer than 128 rows
-// never take a narrower half-key tile, and steps of 2 from 24 to 32 there;
-// 24 or 32 for the wide split.
+// Most sweeps a half-key plan may take: 32, and 36 for the 32-column tile
+// with the even split.  There the streaming role spills 30 registers, and
+// still the 8 selecting waves (16 lanes a column) beat the wide split's 4:
+// 2,300 files, d = 2M, 9.14-9.58 against 11.36-11.40 ms (one process and
+// allocation).  Not with a row table: reading it as well, the streaming
+// role spills 88 registers (15.9 against 12.1 ms with the wide split).
+constexpr int max_half_sweeps(int T, int fill) { return T == 32 && fill == kWsFill ? 36 : 32; }
+
+// Sweep counts built for each plan (sweeps past the last row load nothing,
+// so the count is rounded up only a little).  Half keys: an even count; 8
+// only for 128 columns, where fewer than 128 rows never take a narrower
+// half-key tile, and steps of 2 from 24 to 32 there; 36 for 32 columns
+// (even split); 24 or 32 for the wide split.
 int round_sweeps(int64_t sw, bool half, int T, int fill) {
     if (half) {
         if (fill == kWsFillWide) return sw <= 24 ? 24 : 32;
         if (T == 128 && sw > 24) return (int)((sw + 1) / 2 * 2);
+        if (sw > 32) return 36;   // the 32-column even split only
         return sw <= 8 && T == 128 ? 8 : sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
     }
     return sw <= 2 ? 2 : sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
@@ -1796,7 +1805,7 @@ WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
             if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16)) continue;
             const int64_t rpi = half_rpi(T, fill);
             const int64_t sw = (f + rpi - 1) / rpi;
-            if (sw > 32 || lds(T, fill) > kLdsBytes) continue;
+            if (sw > (ind ? 32 : max_half_sweeps(T, fill)) || lds(T, fill) > kLdsBytes) continue;
             p.T = T;
             p.sweeps = round_sweeps(sw, true, T, fill);
             p.half = true;
@@ -1880,7 +1889,13 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
                 }
                 break;
             case 64: ASPIS_MWS_H(64, kWsFill) break;
-            case 32: ASPIS_MWS_H(32, kWsFill) break;
+            case 32:
+                if (plan.sweeps == 36) {
+                    ASPIS_MWS(32, 36, true, kWsFill)
+                } else {
+                    ASPIS_MWS_H(32, kWsFill)
+                }
+                break;
             case 16: ASPIS_MWS_H(16, kWsFill) break;
             default: return hipErrorInvalidValue;
             }
@@ -1957,13 +1972,13 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     });
     WsPlan best = h.T != 0 ? h : p;
     if (ind) {
-        // a wider tile with the wide split when the row table, read from
-        // global memory (where it stays cached), leaves LDS to the keys:
-        // 2,300 files take 32 columns instead of 16
+        // a wider tile when the row table, read from global memory (where it
+        // stays cached), leaves LDS to the keys: 2,300 files take 32 columns
+        // instead of 16
         WsPlan wide = half_plan(f, best.T, true, true, [&](int T, int fill) {
             return ws_lds_bytes(f, r, T, false, true, fill);
         });
-        if (wide.T != 0 && wide.fill == kWsFillWide) {
+        if (wide.T != 0) {
             wide.rtg = true;
             best = wide;
         }
@@ -1990,8 +2005,8 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
 #define ASPIS_WS1(TT, SWW, II, HH, FF)                                                           \
     fused_ws_kernel<TT, 3, SWW, II, HH, FF><<<grid, kWsThreads, lds, s>>>(                        \
         g, II ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
-#define ASPIS_WS_G(TT, SWW)                                                                      \
-    fused_ws_kernel<TT, 3, SWW, true, true, kWsFillWide, true><<<grid, kWsThreads, lds, s>>>(    \
+#define ASPIS_WS_G(TT, SWW, FF)                                                                  \
+    fused_ws_kernel<TT, 3, SWW, true, true, FF, true><<<grid, kWsThreads, lds, s>>>(             \
         g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
 #define ASPIS_WS(TT, SWW, HH)                         \
     if (ind) {                                        \
@@ -2021,16 +2036,17 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
     case 32: ASPIS_WS1(TT, 32, false, true, kWsFillWide) break;     \
     default: return hipErrorInvalidValue;                           \
     }
-        if (plan.half && plan.fill == kWsFillWide && ind) {
-            if (!plan.rtg) return hipErrorInvalidValue;
-            switch (T * 100 + plan.sweeps) {
-            case 6424: ASPIS_WS_G(64, 24) break;
-            case 6432: ASPIS_WS_G(64, 32) break;
-            case 3224: ASPIS_WS_G(32, 24) break;
-            case 3232: ASPIS_WS_G(32, 32) break;
+        if (plan.rtg) {
+            if (!plan.half) return hipErrorInvalidValue;
+            switch (T * 100 + plan.sweeps + (plan.fill == kWsFillWide ? 10000 : 0)) {
+            case 16424: ASPIS_WS_G(64, 24, kWsFillWide) break;
+            case 16432: ASPIS_WS_G(64, 32, kWsFillWide) break;
+            case 13224: ASPIS_WS_G(32, 24, kWsFillWide) break;
+            case 13232: ASPIS_WS_G(32, 32, kWsFillWide) break;
             default: return hipErrorInvalidValue;
             }
         } else if (plan.half && plan.fill == kWsFillWide) {
+            if (ind) return hipErrorInvalidValue;
             switch (T) {
             case 64: ASPIS_WS_W(64) break;
             case 32: ASPIS_WS_W(32) break;
@@ -2051,7 +2067,15 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
                 }
                 break;
             case 64: ASPIS_WS_H(64) break;
-            case 32: ASPIS_WS_H(32) break;
+            case 32:
+                if (plan.sweeps == 36) {
+                    // a row table in LDS leaves no room for this tile
+                    if (ind) return hipErrorInvalidValue;
+                    ASPIS_WS1(32, 36, false, true, kWsFill)
+                } else {
+                    ASPIS_WS_H(32)
+                }
+                break;
             case 16: ASPIS_WS_H(16) break;
             default: return hipErrorInvalidValue;
             }
