@@ -285,11 +285,13 @@ def _ties_case(K: int, q: int, d: int, kind: str, seed: int):
 @pytest.mark.parametrize("K,q,d,kind", [(11, 2, 132, "equal_high"), (11, 3, 516, "equal_high"),
                                         (12, 2, 264, "two_high"), (11, 2, 260, "signed"),
                                         (12, 3, 132, "signed"), (11, 2, 132, "constant"),
-                                        (21, 2, 68, "equal_high"), (26, 3, 36, "two_high")])
+                                        (21, 2, 68, "equal_high"), (26, 3, 36, "two_high"),
+                                        (25, 2, 36, "equal_high"), (25, 3, 68, "signed")])
 def test_half_key_ties(K, q, d, kind):
     """The half-key tiles (f >= 128: 165 and 220 files in 128-wide tiles,
-    1330 in 32-wide, 2600 in 16-wide), odd and even kept counts (a third
-    adversary drops one file), ragged last tiles, against the oracle."""
+    1330 in 32-wide, 2300 in 32-wide with 36 sweeps, 2600 in 16-wide), odd
+    and even kept counts (a third adversary drops one file), ragged last
+    tiles, against the oracle."""
     g, r = _ties_case(K, q, d, kind, seed=K * 1000 + d)
     print(f"K={K} q={q} d={d} kind={kind}", flush=True)
     for path in ("fused", "two_pass"):
