@@ -364,14 +364,17 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool timing = stats && (flags & ASPIS_FLAG_TIMING);
     aspis_run_stats local{};
-    hipEvent_t ev[6] = {};
+    // timing events, released on every return (error returns included)
+    struct Events {
+        hipEvent_t e[6] = {};
+        ~Events() {
+            for (hipEvent_t x : e)
+                if (x) (void)hipEventDestroy(x);
+        }
+    } events;
+    hipEvent_t *ev = events.e;
     if (timing)
-        for (auto &e : ev) ASPIS_HIP(hipEventCreate(&e));
-    auto destroy = [&]() {
-        if (timing)
-            for (auto &e : ev)
-                if (e) (void)hipEventDestroy(e);
-    };
+        for (int i = 0; i < 6; ++i) ASPIS_HIP(hipEventCreate(&ev[i]));
     std::vector<uint64_t> rows(K);
     auto graph_to_host = [&](aspis_clique_result *out_res) -> aspis_status {
         ASPIS_HIP(hipMemcpyAsync(rows.data(), det->disagree, sizeof(uint64_t) * K,
@@ -412,7 +415,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                                           det->has_majority, det->disagree, ws.stage, s));
         if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
         aspis_clique_result guess{};
-        if ((st = staged_clique(&guess)) != ASPIS_OK) { destroy(); return st; }
+        if ((st = staged_clique(&guess)) != ASPIS_OK) return st;
         // the reduction the guess calls for: the median (Case 2, or MEDIAN
         // mode) or the mean (Case 1 in PAPER mode, or MEAN mode)
         const bool guess_mean = use_mean(mode, &guess);
@@ -435,7 +438,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
             ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
                                               det->has_majority, det->disagree, ws.stage, s));
-            if ((st = staged_clique(res)) != ASPIS_OK) { destroy(); return st; }
+            if ((st = staged_clique(res)) != ASPIS_OK) return st;
             const bool vote_changed = staged[64] != 0;
             // 3) the final selection.  The guess selected the same replica of
             //    every file iff both detections took the same case and
@@ -449,12 +452,10 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 (res->success ? honest_mask(&guess) == honest_mask(res) : !vote_changed);
             const bool hit = same_sel && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
-            if (m == 0) { destroy(); return fail(ASPIS_ERR_NO_FILES, "selection kept no file"); }
-            if (!hit && !use_mean(mode, res) && aspis::pick_median_tile(f) == 0) {
-                destroy();
+            if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
+            if (!hit && !use_mean(mode, res) && aspis::pick_median_tile(f) == 0)
                 return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
                             (long long)aspis::median_capacity(4));
-            }
             // the workspace describes the final selection from here on (the
             // rows and positions a rerun of the reduction reads)
             if (!hit || sel_out)
@@ -478,7 +479,6 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));
                 ASPIS_HIP(hipEventElapsedTime(&local.ms_fallback, ev[4], ev[5]));
             }
-            destroy();
             local.ms_total = std::chrono::duration<float, std::milli>(clk::now() - t0).count();
             if (stats) *stats = local;
             return ASPIS_OK;
@@ -486,11 +486,8 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     }
     // two-pass: full agreement, clique, then selection and reduction
     if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
-    if ((st = detect_impl(grads, row_of, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) {
-        destroy();
-        return st;
-    }
-    if ((st = graph_to_host(res)) != ASPIS_OK) { destroy(); return st; }
+    if ((st = detect_impl(grads, row_of, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) return st;
+    if ((st = graph_to_host(res)) != ASPIS_OK) return st;
     aspis::TileUse tile{};
     st = aggregate_impl(grads, row_of, K, r, d, subsets_dev, det, res, mode, out, sel_out,
                         n_selected, workspace, ws_bytes, stream, &tile);
@@ -499,7 +496,6 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
     ASPIS_HIP(hipStreamSynchronize(s));
     if (timing) ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));
-    destroy();
     local.ms_total = std::chrono::duration<float, std::milli>(clk::now() - t0).count();
     if (stats) *stats = local;
     return st;
