@@ -424,6 +424,20 @@ def test_no_files_leaves_out_untouched():
     assert (to_np(out) == 7.0).all()
 
 
+@pytest.mark.parametrize("idx", [1, 3])
+@pytest.mark.parametrize("d", [1, 2, 3, 4, 5])
+def test_tiny_d(idx, d):
+    """Vectors shorter than one 16-byte chunk or one tile: d = 1..3 (scalar
+    loads), d = 4 (the warp-specialised kernel on a single tile almost all
+    past the end), d = 5; every path."""
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=d)
+    for path in ("fused", "two_pass", "entry_points"):
+        _check(g, wl.K, wl.r, wl.q, "median", path)
+    _check(g, wl.K, wl.r, wl.q, "paper", "fused")
+
+
 def test_unaligned_rows_use_scalar_loads():
     """d not a multiple of 4 and a tensor that starts 4 bytes into a block."""
     import torch
