@@ -200,7 +200,7 @@ def main() -> int:
     if args.simulate:
         return simulate_tables()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported",
+        print(f"bench.py: the benchmark runs on one GPU; --gpus {args.gpus} is not supported",
               file=sys.stderr)
         return 2
 

@@ -56,7 +56,7 @@ typedef enum {
     ASPIS_REDUCE_PAPER = 2       /* mean on successful detection, else median */
 } aspis_reduce;
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define ASPIS_MAX_K_DEVICE 64    /* K for the device entry points            */
 #define ASPIS_MAX_K_CLIQUE 128   /* K for aspis_clique                       */
 #define ASPIS_MAX_R 7            /* largest (odd) redundancy                 */

@@ -7,7 +7,7 @@
 
 namespace aspis {
 
-// Median tile widths (coordinates per workgroup tile) this build supports.
+// Median tile widths (coordinates per workgroup tile) the kernels support.
 // The tile keeps every kept file's keys for T coordinates in LDS, so the
 // widest tile whose [files x T] key block fits is chosen.
 constexpr int kBlock = 256;                 // threads per workgroup
