@@ -383,11 +383,21 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         return aspis_clique(rows.data(), K, q, out_res);
     };
     aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
-    // the row of every replica in a worker-major upload, in the workspace
-    // (kept alive until the stream has been synchronised below)
+    // the row of every replica in a worker-major upload, in the workspace.
+    // The host copy must outlive the asynchronous upload: the guard, declared
+    // after it and so destroyed before it, waits for the stream on every
+    // return (a no-op after the synchronisations of a normal return)
     std::vector<int32_t> host_rows;
+    struct DrainStream {
+        hipStream_t s;
+        bool armed = false;
+        ~DrainStream() {
+            if (armed) (void)hipStreamSynchronize(s);
+        }
+    } drain{s};
     const int32_t *row_of = nullptr;
     if (worker_major) {
+        drain.armed = true;
         host_rows.resize((size_t)f * r);
         worker_row_table(K, r, host_rows.data());
         ASPIS_HIP(hipMemcpyAsync(ws.row_of, host_rows.data(), host_rows.size() * sizeof(int32_t),
