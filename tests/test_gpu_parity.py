@@ -62,6 +62,18 @@ def test_workloads_small(idx, path, dmap):
     _check(g, wl.K, wl.r, wl.q, "median", path)
 
 
+@pytest.mark.parametrize("mode", ["median", "paper"])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_workloads_repeat_seed(idx, mode):
+    """The paper's repeat seed (50): other honest values, and on workloads 2
+    and 4 another seeded draw of the adversaries."""
+    wl = synth.WORKLOADS[idx]
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=_D4[idx], seed=50)
+    print(f"workload {idx} seed 50 mode={mode}", flush=True)
+    _check(g, wl.K, wl.r, wl.q, mode, "fused")
+
+
 @pytest.mark.parametrize("mode", ["mean", "paper"])
 @pytest.mark.parametrize("idx", [1, 3, 4])
 def test_workloads_small_modes(idx, mode):
