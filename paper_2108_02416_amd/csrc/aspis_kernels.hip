@@ -1071,9 +1071,10 @@ constexpr int kWsThreads = 1024;   // threads of a warp-specialised workgroup
 constexpr int kWsFill = 512;       // threads of the streaming role (default split)
 
 // sweeps per burst of loads: as many as the streaming role's registers hold
-// next to the tile's keys (SW x 4 registers)
+// next to the tile's keys (SW x 4 registers, or SW x 2 with half keys).  The
+// 36-sweep tile spills either way; one sweep per burst spills least
 template <int R, int SW>
-constexpr int ws_batch() { return R == 3 ? (SW > 12 ? 2 : 3) : 1; }
+constexpr int ws_batch() { return R == 3 ? (SW > 32 ? 1 : SW > 12 ? 2 : 3) : 1; }
 
 template <int T, int R, int SW, bool IND, bool HALF, int FILL, bool RTG = false>
 __global__ void __launch_bounds__(kWsThreads)
