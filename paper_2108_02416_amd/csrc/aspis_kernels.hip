@@ -1236,10 +1236,15 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                 }
             }
         };
-        Chunks c0;   // sweep 0 of the next tile, loaded early
-        // the rest of tile t, whose sweep 0 is already in c0; the other
-        // sweeps go in bursts of B, all loads of a burst issued first
+        // sweep 0 of the next tile, loaded early: before the barrier and the
+        // hand-over, so that loads stay in flight meanwhile.  The 36-sweep
+        // tile has no registers to spare for it and loads it with its tile
+        constexpr bool kEarly0 = SW <= 32;
+        Chunks c0;
+        // tile t from its sweep 0 (already in c0, or loaded first); the
+        // other sweeps go in bursts of B, all loads of a burst issued first
         auto stream_rest = [&](int64_t t) __attribute__((always_inline)) {
+            if constexpr (!kEarly0) c0 = load_sweep(t, 0);
             proc_sweep(0, c0);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -1276,20 +1281,18 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                 }
             }
         };
-        // sweep 0 of the next tile is issued before the barrier
-        // and the hand-over, so that loads stay in flight meanwhile
         int64_t t = blockIdx.x;
         if (t < ntiles) {
-            c0 = load_sweep(t, 0);
+            if constexpr (kEarly0) c0 = load_sweep(t, 0);
             stream_rest(t);
         }
-        if (t + gridDim.x < ntiles) c0 = load_sweep(t + gridDim.x, 0);
+        if (kEarly0 && t + gridDim.x < ntiles) c0 = load_sweep(t + gridDim.x, 0);
         if (t < ntiles) put_tile();
         __syncthreads();
         for (; t < ntiles; t += gridDim.x) {
             const int64_t tn = t + gridDim.x;
             if (tn < ntiles) stream_rest(tn);
-            if (tn + gridDim.x < ntiles) c0 = load_sweep(tn + gridDim.x, 0);
+            if (kEarly0 && tn + gridDim.x < ntiles) c0 = load_sweep(tn + gridDim.x, 0);
             __syncthreads();
             if (tn < ntiles) put_tile();
             __syncthreads();
