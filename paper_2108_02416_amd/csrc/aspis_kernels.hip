@@ -1238,8 +1238,9 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
         };
         // sweep 0 of the next tile, loaded early: before the barrier and the
         // hand-over, so that loads stay in flight meanwhile.  The 36-sweep
-        // tile has no registers to spare for it and loads it with its tile
-        constexpr bool kEarly0 = SW <= 32;
+        // tile and the row-table reads have no registers to spare for it and
+        // load it with their tile
+        constexpr bool kEarly0 = SW <= 32 && !IND;
         Chunks c0;
         // tile t from its sweep 0 (already in c0, or loaded first); the
         // other sweeps go in bursts of B, all loads of a burst issued first
