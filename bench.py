@@ -15,7 +15,9 @@ step / step time).  `roofline` reports the dominant kernel (the single-pass
 agreement + median kernel) from HIP events recorded on its stream inside the
 library; `read_ceiling` is a linear read of the same tensor with the same
 loads (the part's ceiling for this allocation); `cpu_baseline` times the
-oracle on a bounded coordinate sample of the same workload on the host.
+oracle on the host over the same replicas: one thread on a coordinate slice,
+and every coordinate on the host's threads, whose output is compared with
+the GPU's (`parity_all_coordinates`).
 """
 from __future__ import annotations
 
@@ -65,40 +67,95 @@ def measured_traffic(per_launch_bytes_alg: float):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, role, worker, sample_coords: int, gpu_out, gpu_sel, mode: str = "median"):
-    """The oracle, as it stands, on coordinates [0, sample_coords) of the
-    workload (single thread); returns the JSON object and a parity verdict."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            return next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
+                        None)
+    except OSError:
+        return None
+
+
+def cpu_baseline(torch, wl, chunk_of, d, gpu_out, gpu_sel, sample_coords: int, full: bool,
+                 mode: str = "median"):
+    """The oracle, as it stands, timed on the host's cores over the same
+    replicas the GPU step consumed (chunk_of(k0, n) reads coordinates
+    [k0, k0+n) of every replica back from the device tensor as float32
+    [f, r, n]; the read-back is not timed):
+
+      single   one thread, coordinates [0, sample_coords) (Algorithm 3
+               then Algorithm 1 on that slice, as one call of oracle.run)
+      full     every coordinate on min(16, nproc) threads through the
+               chunk-parallel driver: agreement over all d (pass 1), then
+               detection and selection, then the reduction (pass 2)
+
+    Returns the cpu_baseline object and the parity verdicts (the oracle's
+    output against the GPU's: on the slice, and on every coordinate)."""
     import numpy as np
 
     import oracle
-    import synth
+    from oracle import parallel as oracle_parallel
 
-    s = oracle.assign(wl.K, wl.r)
-    g = synth.fill(role, worker, 0, sample_coords, wl.dist, alie_z=wl.alie_z)
+    K, r, q, f = wl.K, wl.r, wl.q, wl.f
+
+    def same(got, ref, by_mean):
+        if not by_mean:
+            return bool(np.array_equal(got.view(np.uint32), ref.view(np.uint32)))
+        ref = ref.astype(np.float64)
+        return bool(np.all(np.abs(got.astype(np.float64) - ref)
+                           <= 1e-6 * np.maximum(np.abs(ref), 1e-30)))
+
+    n1 = min(sample_coords, d)
+    g = chunk_of(0, n1)
     t0 = time.perf_counter()
-    res = oracle.run(g, wl.K, wl.r, wl.q, mode=mode)
-    dt = time.perf_counter() - t0
-    value = g.nbytes / dt / 1e9
-    same_sel = bool(np.array_equal(res["sel"], gpu_sel))
-    got = gpu_out[:sample_coords]
-    if res["out"].dtype == np.float32 and mode == "median":
-        same_out = same_sel and bool(np.array_equal(res["out"].view(np.uint32), got.view(np.uint32)))
-    else:   # a mean: within 1e-6 relative of the oracle's fp64 sum
-        ref = res["out"].astype(np.float64)
-        same_out = same_sel and bool(np.all(np.abs(got.astype(np.float64) - ref)
-                                            <= 1e-6 * np.maximum(np.abs(ref), 1e-30)))
-    model = None
-    try:
-        with open("/proc/cpuinfo") as fh:
-            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")),
-                         None)
-    except OSError:
-        pass
-    return ({"value": round(value, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-             "cpu_model": model,
-             "sample": f"coordinates [0,{sample_coords}) of the same workload "
-                       f"({g.nbytes / 1e9:.2f} GB of replicas), {dt:.1f} s single-threaded"},
-            same_out)
+    res = oracle.run(g, K, r, q, mode=mode)
+    dt1 = time.perf_counter() - t0
+    slice_mean = mode == "mean" or (mode == "paper" and res["clique"]["success"])
+    parity_slice = bool(np.array_equal(res["sel"], gpu_sel)) and \
+        same(gpu_out[:n1], res["out"], slice_mean)
+    single = {"value": round(g.nbytes / dt1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+              "seconds": round(dt1, 2),
+              "sample": f"coordinates [0,{n1}) ({g.nbytes / 1e9:.2f} GB of replicas), one thread"}
+    del g
+    out = {"kind": "oracle", "cpu_model": _cpu_model(), "single_thread": single}
+    parity_full = None
+    if full:
+        nthreads = oracle_parallel.workers()
+        s = oracle.assign(K, r)
+        step = max(1024, (1 << 30) // (f * r * 4))
+        timed = 0.0
+        alpha = np.ones((f, r * (r - 1) // 2), dtype=np.uint8)
+        for k0 in range(0, d, step):
+            n = min(step, d - k0)
+            h = chunk_of(k0, n)
+            t0 = time.perf_counter()
+            alpha &= oracle_parallel.agreement(h, nthreads)
+            timed += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        det = oracle.detect(None, s, K, q, alpha=alpha)
+        cl = det["clique"]
+        sel, kept = oracle.select(s, det["vote"], cl["success"], cl["honest"])
+        by_mean = mode == "mean" or (mode == "paper" and cl["success"])
+        reduce_fn = (oracle_parallel.mean_by_coordinates if by_mean
+                     else oracle_parallel.median_by_coordinates)
+        timed += time.perf_counter() - t0
+        parity_full = bool(np.array_equal(sel, gpu_sel))
+        for k0 in range(0, d, step):
+            n = min(step, d - k0)
+            h = chunk_of(k0, n)
+            t0 = time.perf_counter()
+            o = reduce_fn(h, sel, nthreads)
+            timed += time.perf_counter() - t0
+            parity_full = parity_full and same(gpu_out[k0:k0 + n], o, by_mean)
+        nbytes = float(f * r * d * 4)
+        out.update({"value": round(nbytes / timed / 1e9, 4), "unit": "GB/s", "cores": nthreads,
+                    "seconds": round(timed, 2),
+                    "sample": f"the whole workload: all {d} coordinates, {nbytes / 1e9:.2f} GB "
+                              f"of replicas, on {nthreads} threads (chunk-parallel driver; "
+                              f"device read-back not timed)"})
+    else:
+        out.update({k: single[k] for k in ("value", "unit", "cores", "sample")})
+    return out, parity_slice, parity_full
 
 
 def read_ceiling(torch, aspis, grads, reps: int = 5) -> dict:
@@ -188,7 +245,15 @@ def main() -> int:
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the linear read of the replica tensor after the timed steps")
     ap.add_argument("--cpu-sample", type=int, default=1 << 20,
-                    help="coordinates of the oracle's CPU-baseline sample (0 = skip)")
+                    help="coordinates of the oracle's single-threaded CPU-baseline slice "
+                         "(0 = skip the CPU baseline)")
+    ap.add_argument("--no-cpu-full", action="store_true",
+                    help="skip the oracle over every coordinate on the host's threads")
+    ap.add_argument("--adversary-late", type=int, default=0, metavar="P",
+                    help="the adversaries send honest values on coordinates [0, P) and distort "
+                         "only after (Section 4.2's adversary, who knows the protocol): with P "
+                         "beyond the probed prefix every step's guess misses and the median is "
+                         "rerun (0 = off; 65536 is past any prefix)")
     ap.add_argument("--simulate", action="store_true",
                     help="instead of the step, run the host distortion-fraction simulator over "
                          "the paper's tables (K=15, 21, 24), the K=50 sweep and the K=100, r=5 "
@@ -226,6 +291,16 @@ def main() -> int:
     t_gen = time.perf_counter()
     grads = torch.empty((f, r, d), dtype=torch.float32, device=dev)
     synth.fill_device(role, worker, grads, wl.dist, seed=args.seed, alie_z=wl.alie_z)
+    if args.adversary_late > 0:
+        # the same generator with every replica honest, over the first P
+        # coordinates (it is counter-based: coordinate k has the same value
+        # in a tensor of any length)
+        P = min(args.adversary_late, d)
+        clean = torch.empty((f, r, P), dtype=torch.float32, device=dev)
+        synth.fill_device(np.zeros_like(role), worker, clean, wl.dist, seed=args.seed,
+                          alie_z=wl.alie_z)
+        grads[:, :, :P].copy_(clean)
+        del clean
     if args.layout == "worker":
         # the same replicas in the order the workers upload them
         l_files = f * r // K
@@ -294,11 +369,32 @@ def main() -> int:
         ceiling["kernel_frac"] = round(achieved / ceiling["GB/s"], 4)
         ceiling["step_frac"] = round(value / ceiling["GB/s"], 4)
 
+    fallback = None
+    if last["fused"] and not last["speculation_hit"]:
+        ms_fb = float(np.mean([s["ms_fallback"] for s in stats]))
+        fb_bytes = step_out["n_selected"] * d * 4.0 + d * 4.0
+        fallback = {"kernel": f"{red} rerun over the final selection"
+                              + (f" ({last['tile_cols']}-column tiles)" if not by_mean else ""),
+                    "ms": round(ms_fb, 4), "algorithmic_bytes": fb_bytes,
+                    "achieved": round(fb_bytes / (ms_fb / 1e3) / 1e9, 1), "unit": "GB/s",
+                    "frac": round(fb_bytes / (ms_fb / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+
     cpu = None
-    parity = None
+    parity = {}
     if args.cpu_sample > 0:
-        cpu, parity = cpu_baseline(wl, role, worker, min(args.cpu_sample, d),
-                                   out.cpu().numpy(), sel.cpu().numpy(), args.mode)
+        if args.layout == "file":
+            def chunk_of(k0, n):
+                return grads[:, :, k0:k0 + n].contiguous().cpu().numpy()
+        else:
+            rows_fm = torch.from_numpy(aspis.worker_rows(K, r).reshape(-1).astype(np.int64)).to(dev)
+            flat = grads.view(-1, d)
+
+            def chunk_of(k0, n):
+                return flat[:, k0:k0 + n].index_select(0, rows_fm).view(f, r, n).cpu().numpy()
+        cpu, p_slice, p_full = cpu_baseline(torch, wl, chunk_of, d, out.cpu().numpy(),
+                                            sel.cpu().numpy(), args.cpu_sample,
+                                            not args.no_cpu_full, args.mode)
+        parity = {"parity_on_cpu_sample": p_slice, "parity_all_coordinates": p_full}
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
@@ -308,6 +404,8 @@ def main() -> int:
                  + ("Student-t(3)" if wl.dist == synth.DIST_STUDENT3 else "Irwin-Hall N(0,0.01^2)")
                  + f" honest gradients, {wl.distortion} adversaries"),
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
+                   **({"adversary_late": min(args.adversary_late, d)}
+                      if args.adversary_late > 0 else {}),
                    "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
                    **({"alie_z": wl.alie_z} if "alie" in wl.distortion else {}),
@@ -318,9 +416,10 @@ def main() -> int:
                  "ms_fallback": round(last["ms_fallback"], 4),
                  "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"])},
         "roofline": roofline,
+        "fallback": fallback,
         "read_ceiling": ceiling,
         "cpu_baseline": cpu,
-        "parity_on_cpu_sample": parity,
+        **parity,
     }
     print(json.dumps(line), flush=True)
     return 0

@@ -28,8 +28,9 @@
  * the stream (it needs the agreement graph on the host) and returns with
  * its work complete.
  *
- * Thread safety: re-entrant; the only global state is the per-thread error
- * message.  Calls that share output buffers must not overlap.
+ * Thread safety: re-entrant.  Global state: the per-thread error message
+ * and a per-device cache of the compute-unit count (written once per device
+ * with relaxed atomics).  Calls that share output buffers must not overlap.
  */
 #ifndef ASPIS_H
 #define ASPIS_H
@@ -226,6 +227,36 @@ aspis_status aspis_detect_aggregate_wm(const float *grads_wm, int32_t K, int32_t
                                        int64_t *n_selected, void *workspace,
                                        size_t ws_bytes, uint32_t flags,
                                        aspis_run_stats *stats, void *stream);
+
+/* The kernels the device entry points take for a shape, decided without
+ * launching anything (host only; assumes a 16-byte aligned tensor).
+ *   single_pass  the single-pass kernel of aspis_detect_aggregate (worker-
+ *                major: aspis_detect_aggregate_wm) for the median, or
+ *                ASPIS_KERNEL_NONE when the shape takes the two-pass path
+ *   median       the median kernel of aspis_aggregate and of the rerun
+ *                after a wrong guess (for up to f kept files)
+ * Errors: INVALID_ARG for an invalid shape (as aspis_detect) or when a
+ * planned kernel is not built (the launch would fail the same way). */
+#define ASPIS_KERNEL_NONE 0          /* no kernel: the step takes two passes    */
+#define ASPIS_KERNEL_FUSED_WS 1      /* single pass, warp-specialised           */
+#define ASPIS_KERNEL_FUSED 2         /* single pass, load then select per tile  */
+#define ASPIS_KERNEL_MEDIAN_WS 3     /* median, warp-specialised                */
+#define ASPIS_KERNEL_MEDIAN_TILE 4   /* median, LDS key tile                    */
+#define ASPIS_KERNEL_MEDIAN_RADIX 5  /* median, radix select re-reading HBM     */
+typedef struct {
+    int32_t kernel;           /* ASPIS_KERNEL_*                                */
+    int32_t tile_cols;        /* coordinates per tile                          */
+    int32_t sweeps;           /* streaming sweeps per tile (warp-specialised)  */
+    int32_t half_keys;        /* 1: the tile keeps the high 16 bits of keys    */
+    int32_t stream_threads;   /* threads of the streaming role                 */
+    int32_t row_table;        /* 0 none, 1 staged in LDS, 2 global memory      */
+    int32_t block;            /* threads per workgroup                         */
+    int32_t reserved;
+    int64_t lds_bytes;        /* dynamic LDS per workgroup (0: static only)    */
+} aspis_kernel_plan;
+
+aspis_status aspis_plan(int32_t K, int32_t r, int64_t d, int32_t worker_major,
+                        aspis_kernel_plan *single_pass, aspis_kernel_plan *median);
 
 /* Diagnostic: streams nbytes (multiple of 16) of device memory and writes a
  * checksum word per thread to sink (device, >= aspis_read_probe_sink_words()

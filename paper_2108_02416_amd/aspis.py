@@ -26,7 +26,7 @@ FLAG_TIMING = 2
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
     "aspis_aggregate_workspace", "aspis_aggregate", "aspis_detect_aggregate",
-    "aspis_detect_aggregate_wm", "aspis_worker_rows",
+    "aspis_detect_aggregate_wm", "aspis_worker_rows", "aspis_plan",
     "aspis_read_probe_sink_words", "aspis_read_probe", "aspis_simulate", "aspis_detox",
     "aspis_last_error",
 )
@@ -84,6 +84,23 @@ class RunStats(ctypes.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+KERNEL = {0: "none", 1: "fused_ws", 2: "fused", 3: "median_ws", 4: "median_tile",
+          5: "median_radix"}
+
+
+class KernelPlan(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("tile_cols", ctypes.c_int32),
+                ("sweeps", ctypes.c_int32), ("half_keys", ctypes.c_int32),
+                ("stream_threads", ctypes.c_int32), ("row_table", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int64)]
+
+    def as_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d["kernel"] = KERNEL.get(self.kernel, str(self.kernel))
+        return d
+
+
 _lib = None
 
 
@@ -123,6 +140,9 @@ def lib():
     L.aspis_detect_aggregate_wm.restype = ctypes.c_int
     L.aspis_worker_rows.argtypes = [i32, i32, P, i64]
     L.aspis_worker_rows.restype = ctypes.c_int
+    L.aspis_plan.argtypes = [i32, i32, i64, i32, ctypes.POINTER(KernelPlan),
+                             ctypes.POINTER(KernelPlan)]
+    L.aspis_plan.restype = ctypes.c_int
     L.aspis_read_probe_sink_words.argtypes = []
     L.aspis_read_probe_sink_words.restype = ctypes.c_size_t
     L.aspis_read_probe.argtypes = [P, ctypes.c_size_t, P, P]
@@ -167,6 +187,15 @@ def worker_rows(K: int, r: int) -> np.ndarray:
     out = np.zeros((f, r), dtype=np.int32)
     _check(lib().aspis_worker_rows(K, r, out.ctypes.data, f * r))
     return out
+
+
+def plan(K: int, r: int, d: int, layout: str = "file") -> tuple[dict, dict]:
+    """The kernels the device entry points take for this shape (aspis_plan):
+    (single pass, median), each a dict of the kernel's tile parameters."""
+    sp, med = KernelPlan(), KernelPlan()
+    _check(lib().aspis_plan(K, r, d, 1 if layout == "worker" else 0, ctypes.byref(sp),
+                            ctypes.byref(med)))
+    return sp.as_dict(), med.as_dict()
 
 
 def clique(disagree_rows: np.ndarray, K: int, q: int) -> CliqueResult:
@@ -230,6 +259,34 @@ def _check_grads(grads, K: int, r: int):
     return f, grads.shape[2]
 
 
+def _check_buffer(name: str, t, dtype, n: int, device):
+    """A caller-supplied buffer must be a contiguous tensor of `dtype` with at
+    least n elements on the replicas' device: the kernels write n elements."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise AspisError(ERR_INVALID_ARG, f"{name} must be a torch tensor")
+    if t.dtype != dtype or not t.is_contiguous() or t.device != device or t.numel() < n:
+        raise AspisError(ERR_INVALID_ARG,
+                         f"{name} must be a contiguous {dtype} tensor on {device} with at "
+                         f"least {n} elements (got {t.dtype}, {tuple(t.shape)}, {t.device}, "
+                         f"contiguous={t.is_contiguous()})")
+
+
+def _check_outputs(device, f: int, K: int, d: int, bufs=None, out=None, sel_out=None, ws=None):
+    torch = _torch()
+    if bufs is not None:
+        _check_buffer("bufs.pair_diff", bufs.pair_diff, torch.int32, f, device)
+        _check_buffer("bufs.vote", bufs.vote, torch.int8, f, device)
+        _check_buffer("bufs.has_majority", bufs.has_majority, torch.uint8, f, device)
+        _check_buffer("bufs.disagree", bufs.disagree, torch.int64, K, device)
+    if out is not None:
+        _check_buffer("out", out, torch.float32, d, device)
+    if sel_out is not None:
+        _check_buffer("sel_out", sel_out, torch.int32, f, device)
+    if ws is not None:
+        _check_buffer("ws", ws, torch.uint8, 1, device)
+
+
 @dataclass
 class DetectBuffers:
     pair_diff: object
@@ -278,6 +335,7 @@ def _aligned_ptr(ws) -> tuple[int, int]:
 def detect(grads, K: int, r: int, bufs: DetectBuffers | None = None) -> DetectBuffers:
     f, d = _check_grads(grads, K, r)
     bufs = bufs or DetectBuffers.empty(f, K, grads.device)
+    _check_outputs(grads.device, f, K, d, bufs=bufs)
     sub = subsets_device(K, r, grads.device)
     out = bufs.c()
     _check(lib().aspis_detect(grads.data_ptr(), K, r, d, sub.data_ptr(), ctypes.byref(out),
@@ -291,6 +349,7 @@ def aggregate(grads, K: int, r: int, bufs: DetectBuffers, res: CliqueResult,
     f, d = _check_grads(grads, K, r)
     out = out if out is not None else torch.empty(d, dtype=torch.float32, device=grads.device)
     ws = ws if ws is not None else workspace(K, r, d, grads.device)
+    _check_outputs(grads.device, f, K, d, bufs=bufs, out=out, sel_out=sel_out, ws=ws)
     wp, wn = _aligned_ptr(ws)
     n_sel = ctypes.c_int64(0)
     det = bufs.c()
@@ -329,6 +388,7 @@ def detect_aggregate(grads, K: int, r: int, q: int, mode: str = "median", flags:
     if sel_out is None and want_sel:
         sel_out = torch.empty(f, dtype=torch.int32, device=grads.device)
     ws = ws if ws is not None else workspace(K, r, d, grads.device)
+    _check_outputs(grads.device, f, K, d, bufs=bufs, out=out, sel_out=sel_out, ws=ws)
     wp, wn = _aligned_ptr(ws)
     res = CliqueResult()
     stats = RunStats()

@@ -321,9 +321,6 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
     const int64_t m = kept_files(K, r, f, res);
     if (n_selected) *n_selected = m;
     const bool mean = use_mean(mode, res);
-    if (!mean && aspis::pick_median_tile(f) == 0)
-        return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
-                    (long long)aspis::median_capacity(4));
     hipStream_t s = static_cast<hipStream_t>(stream);
     aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
     ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success, honest_mask(res),
@@ -357,10 +354,6 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         return fail(ASPIS_ERR_BUFFER_SMALL, "workspace needs %zu bytes", aspis::workspace_bytes(f, r));
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ASPIS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-    // PAPER needs the median only when detection fails: checked once known
-    if (mode == ASPIS_REDUCE_MEDIAN && aspis::pick_median_tile(f) == 0)
-        return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
-                    (long long)aspis::median_capacity(4));
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool timing = stats && (flags & ASPIS_FLAG_TIMING);
     aspis_run_stats local{};
@@ -463,9 +456,6 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             const bool hit = same_sel && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
-            if (!hit && !use_mean(mode, res) && aspis::pick_median_tile(f) == 0)
-                return fail(ASPIS_ERR_INVALID_ARG, "median supports at most %lld files",
-                            (long long)aspis::median_capacity(4));
             // the workspace describes the final selection from here on (the
             // rows and positions a rerun of the reduction reads)
             if (!hit || sel_out)
@@ -559,6 +549,44 @@ aspis_status aspis_worker_rows(int32_t K, int32_t r, int32_t *row_of, int64_t ca
         return fail(ASPIS_ERR_BUFFER_SMALL, "need %lld entries, buffer holds %lld",
                     (long long)(f * r), (long long)cap_entries);
     worker_row_table(K, r, row_of);
+    return ASPIS_OK;
+}
+
+static_assert(ASPIS_KERNEL_NONE == aspis::kKernelNone && ASPIS_KERNEL_FUSED_WS == aspis::kKernelFusedWs &&
+                  ASPIS_KERNEL_FUSED == aspis::kKernelFused &&
+                  ASPIS_KERNEL_MEDIAN_WS == aspis::kKernelMedianWs &&
+                  ASPIS_KERNEL_MEDIAN_TILE == aspis::kKernelMedianTile &&
+                  ASPIS_KERNEL_MEDIAN_RADIX == aspis::kKernelMedianRadix,
+              "kernel kinds of aspis.h and the launchers");
+
+static void to_abi(const aspis::KernelPlan &k, aspis_kernel_plan *out) {
+    out->kernel = k.kind;
+    out->tile_cols = k.tile_cols;
+    out->sweeps = k.sweeps;
+    out->half_keys = k.half_keys;
+    out->stream_threads = k.stream_threads;
+    out->row_table = k.row_table;
+    out->block = k.block;
+    out->reserved = 0;
+    out->lds_bytes = k.lds_bytes;
+}
+
+aspis_status aspis_plan(int32_t K, int32_t r, int64_t d, int32_t worker_major,
+                        aspis_kernel_plan *single_pass, aspis_kernel_plan *median) {
+    int64_t f = 0;
+    aspis_status st = check_device_shape(K, r, d, &f);
+    if (st != ASPIS_OK) return st;
+    if (!single_pass || !median) return fail(ASPIS_ERR_INVALID_ARG, "aspis_plan: NULL output");
+    const bool vec = d % 4 == 0;
+    aspis::KernelPlan fused{}, med{};
+    if (f <= aspis::kVoteRowsMaxFiles) aspis::plan_fused(f, r, vec, worker_major != 0, &fused);
+    aspis::plan_median(f, vec, &med);
+    to_abi(fused, single_pass);
+    to_abi(med, median);
+    if (fused.kind == aspis::kKernelUnbuilt || med.kind == aspis::kKernelUnbuilt)
+        return fail(ASPIS_ERR_INVALID_ARG, "aspis_plan: K=%d r=%d d=%lld: a planned kernel is not built",
+                    K, r, (long long)d);
+    g_err[0] = 0;
     return ASPIS_OK;
 }
 

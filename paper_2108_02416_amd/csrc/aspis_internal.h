@@ -19,9 +19,6 @@ constexpr int kHistBuckets = 128;
 constexpr int kHistStride = 132;
 constexpr int64_t hist_bytes(int T) { return (int64_t)T * kHistStride * 4; }
 
-// Largest number of kept files the LDS-tiled median supports for tile T.
-inline int64_t median_capacity(int T) { return (kLdsBytes - hist_bytes(T)) / (4 * (int64_t)T); }
-
 // Workspace layout (byte offsets) for f files.
 struct Workspace {
     int32_t *sel;     // [f] kept slot or -1
@@ -73,15 +70,37 @@ hipError_t launch_select(const int32_t *subsets, const int8_t *vote,
                          const int32_t *row_of, const Workspace &ws,
                          int32_t *sel_out, uint32_t *zero, int64_t n_zero, hipStream_t s);
 
-// Tile width the median kernel uses for up to f kept files (0: too many).
-int pick_median_tile(int64_t f);
-
 // Tile a median kernel ran with: columns per tile, and whether the tile
 // kept only the high halves of the keys.
 struct TileUse {
     int32_t cols = 0;
     int32_t half = 0;
 };
+
+// The kernel a launcher takes for a shape, decided without launching
+// (the values of ASPIS_KERNEL_* in aspis.h).
+constexpr int32_t kKernelNone = 0;          // no kernel of this kind for the shape
+constexpr int32_t kKernelFusedWs = 1;       // fused_ws_kernel (warp-specialised single pass)
+constexpr int32_t kKernelFused = 2;         // fused_kernel (single pass, load then select)
+constexpr int32_t kKernelMedianWs = 3;      // median_ws_kernel
+constexpr int32_t kKernelMedianTile = 4;    // median_kernel (LDS key tile)
+constexpr int32_t kKernelMedianRadix = 5;   // median_radix_kernel (keys re-read from HBM)
+constexpr int32_t kKernelUnbuilt = -1;      // planned, but no kernel is built for the plan
+struct KernelPlan {
+    int32_t kind = kKernelNone;
+    int32_t tile_cols = 0;        // coordinates per tile
+    int32_t sweeps = 0;           // streaming sweeps per tile (warp-specialised kernels)
+    int32_t half_keys = 0;        // the tile keeps only the high 16 bits of each key
+    int32_t stream_threads = 0;   // threads of the streaming role (warp-specialised)
+    int32_t row_table = 0;        // 0 none, 1 staged in LDS, 2 read from global memory
+    int32_t block = 0;            // threads per workgroup
+    int64_t lds_bytes = 0;        // dynamic LDS per workgroup
+};
+// Median over up to f kept rows (always has a kernel); single pass for f
+// files of r replicas (false: none, the step then takes two passes).  vec:
+// d % 4 == 0 and a 16-byte aligned tensor; ind: rows through a row table.
+bool plan_median(int64_t f, bool vec, KernelPlan *out);
+bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out);
 
 // Coordinate-wise lower median / fp64 mean of the kept rows.
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,

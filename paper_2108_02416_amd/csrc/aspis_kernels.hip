@@ -40,6 +40,7 @@
 //                      order.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 
 #include "aspis_internal.h"
@@ -1589,6 +1590,96 @@ mean_kernel(const float *__restrict__ g, int64_t d,
 }
 
 // ---------------------------------------------------------------------------
+// median of any number of kept rows: an MSB-first radix select over the
+// 32-bit keys in four rounds of 8 bits, whose histograms live in LDS while
+// the keys are read from HBM again in every round.  It takes over when not
+// even a narrow tile of every kept row's keys fits in LDS (beyond about
+// 10,000 kept files); it reads the kept rows four times, trading bandwidth
+// for capacity.  Lane c of every wave owns column c of a 64-column tile and
+// wave w reads rows w, w + 4, ... (256-byte row segments per wave load).
+
+constexpr int kRadixCols = 64;
+constexpr int kRadixThreads = 256;
+constexpr int kRadixWaves = kRadixThreads / kRadixCols;
+constexpr int kRadixBuckets = 256;
+constexpr int kRadixStride = kRadixBuckets + 1;   // bucket b of column c at c*257 + b:
+                                                  // bank (c + b) % 64
+constexpr int kRadixBatch = 8;                    // row loads in flight per lane
+constexpr int kRadixQuarter = kRadixBuckets / kRadixWaves;
+
+__global__ void __launch_bounds__(kRadixThreads)
+median_radix_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
+                    const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
+    __shared__ uint32_t hist[kRadixCols * kRadixStride];
+    __shared__ uint32_t part[kRadixWaves][kRadixCols];   // bucket counts per quarter
+    __shared__ uint32_t prefix[kRadixCols], rank[kRadixCols];
+    const int n = *n_sel;
+    if (n <= 0) return;   // uniform: no workgroup reaches a barrier
+    const int tid = threadIdx.x, c = tid % kRadixCols, w = tid / kRadixCols;
+    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const int64_t k = t * kRadixCols + c;
+        const bool valid = k < d;
+        if (tid < kRadixCols) {
+            prefix[tid] = 0u;
+            rank[tid] = (uint32_t)(n - 1) / 2;
+        }
+        // round x settles key bits [24 - 8x, 32 - 8x) among the keys whose
+        // higher bits equal the prefix settled so far
+        for (int round = 0; round < 4; ++round) {
+            for (int i = tid; i < kRadixCols * kRadixStride; i += kRadixThreads) hist[i] = 0u;
+            __syncthreads();
+            const int sh = 24 - 8 * round;
+            const uint32_t pre = prefix[c];
+            uint32_t *hc = hist + c * kRadixStride;
+            auto count = [&](uint32_t v) __attribute__((always_inline)) {
+                const uint32_t key = to_key(v);
+                if (round == 0 || (key >> (sh + 8)) == pre) atomicAdd(&hc[(key >> sh) & 255u], 1u);
+            };
+            if (valid) {
+                const float *col = g + k;
+                int j = w;
+                for (; j + (kRadixBatch - 1) * kRadixWaves < n; j += kRadixBatch * kRadixWaves) {
+                    uint32_t v[kRadixBatch];
+#pragma unroll
+                    for (int u = 0; u < kRadixBatch; ++u)
+                        v[u] = __float_as_uint(col[(int64_t)rows[j + u * kRadixWaves] * d]);
+#pragma unroll
+                    for (int u = 0; u < kRadixBatch; ++u) count(v[u]);
+                }
+                for (; j < n; j += kRadixWaves) count(__float_as_uint(col[(int64_t)rows[j] * d]));
+            }
+            __syncthreads();
+            // the bucket holding the sought rank: wave w sums its quarter of
+            // the column's buckets, then one lane per column walks the
+            // quarters and the buckets of the quarter that holds it
+            uint32_t sum = 0u;
+#pragma unroll 8
+            for (int b = 0; b < kRadixQuarter; ++b) sum += hc[w * kRadixQuarter + b];
+            part[w][c] = sum;
+            __syncthreads();
+            if (tid < kRadixCols) {
+                uint32_t m = rank[c], run = 0u;
+                int qt = 0;
+                for (; qt < kRadixWaves - 1; ++qt) {
+                    if (run + part[qt][c] > m) break;
+                    run += part[qt][c];
+                }
+                int b = qt * kRadixQuarter;
+                for (; b < (qt + 1) * kRadixQuarter - 1; ++b) {
+                    if (run + hc[b] > m) break;
+                    run += hc[b];
+                }
+                rank[c] = m - run;
+                prefix[c] = (prefix[c] << 8) | (uint32_t)b;
+            }
+            __syncthreads();
+        }
+        if (w == 0 && valid) out[k] = __uint_as_float(from_key(prefix[c]));
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
 // read-bandwidth probe
 
 constexpr int kProbeBlocks = 2048;
@@ -1604,20 +1695,22 @@ read_probe_kernel(const uint4 *__restrict__ p, int64_t n16, uint32_t *sink) {
     sink[blockIdx.x * (int64_t)blockDim.x + threadIdx.x] = acc;
 }
 
-int g_num_cus = 0;
+// Compute units of each device, looked up once per device (relaxed atomics:
+// concurrent first calls store the same value).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_num_cus[kMaxDevices];
 
 int num_cus() {
-    if (g_num_cus == 0) {
-        int dev = 0, cus = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) ==
-                hipSuccess &&
-            cus > 0)
-            g_num_cus = cus;
-        else
-            g_num_cus = 256;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int cus = g_num_cus[dev].load(std::memory_order_relaxed);
+    if (cus == 0) {
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        g_num_cus[dev].store(cus, std::memory_order_relaxed);
     }
-    return g_num_cus;
+    return cus;
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -1651,8 +1744,6 @@ size_t workspace_bytes(int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
     return up((size_t)f * 4) * 3 + kWsCounters + kWsStage + up((size_t)f * r * 4);
 }
-
-int pick_median_tile(int64_t f) { return pick_tile(f, 0); }
 
 Workspace carve_workspace(void *base, int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -1750,6 +1841,8 @@ hipError_t launch_select(const int32_t *subsets, const int8_t *vote, int64_t f, 
     return hipGetLastError();
 }
 
+namespace {
+
 // Warp-specialised plans.  Full keys: the widest tile (8..64 columns) whose
 // key block fits in LDS and whose rows fit the streaming role's registers
 // (at most 16 sweeps of 4 key registers).  Half keys, for many rows: a wider
@@ -1801,7 +1894,10 @@ int round_sweeps(int64_t sw, bool half, int T, int fill) {
 // registers of the streaming role next to 30 sweeps of keys, and still
 // beats the 64-column full-key tile (10.9 against 11.6 ms at 455 files,
 // d = 11.2M, one process and allocation).  A row table staged in LDS rules
-// out the wide split; one read from global memory (rtg) does not.
+// out the wide split; one read from global memory (rtg) takes the wide
+// split only: with the even split the streaming role would hold the
+// table's addresses next to its keys (the kernels built for a global
+// table are wide-split ones).
 template <typename LdsFn>
 WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
     WsPlan p;
@@ -1810,6 +1906,7 @@ WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
         if (T <= narrower) break;
         for (int fill : {kWsFill, kWsFillWide}) {
             if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16)) continue;
+            if (rtg && fill != kWsFillWide) continue;
             const int64_t rpi = half_rpi(T, fill);
             const int64_t sw = (f + rpi - 1) / rpi;
             if (sw > (ind ? 32 : max_half_sweeps(T, fill)) || lds(T, fill) > kLdsBytes) continue;
@@ -1817,6 +1914,7 @@ WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
             p.sweeps = round_sweeps(sw, true, T, fill);
             p.half = true;
             p.fill = fill;
+            p.rtg = rtg;
             return p;
         }
     }
@@ -1848,120 +1946,17 @@ WsPlan mws_plan(int64_t f, bool vec) {
     return h.T != 0 ? h : p;
 }
 
-hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
-                         float *out, hipStream_t s, TileUse *use) {
-    const bool vec_ws = (d % 4 == 0) && aligned16(g);
-    const WsPlan plan = mws_plan(f, vec_ws);
-    if (use) *use = TileUse{plan.T, plan.half ? 1 : 0};
-    if (plan.T != 0) {
-        const int T = plan.T;
-        const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)mws_lds_bytes(f, T, plan.half, plan.fill);
-        const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_MWS(TT, SWW, HH, FF)                                                           \
-    median_ws_kernel<TT, SWW, HH, FF><<<grid, kWsThreads, lds, s>>>(g, d, ws.rows, ws.n_sel,  \
-                                                                    ntiles, out);
-#define ASPIS_MWS_T(TT)                                  \
-    switch (plan.sweeps) {                               \
-    case 4: ASPIS_MWS(TT, 4, false, kWsFill) break;      \
-    case 8: ASPIS_MWS(TT, 8, false, kWsFill) break;      \
-    case 12: ASPIS_MWS(TT, 12, false, kWsFill) break;    \
-    default: return hipErrorInvalidValue;                \
-    }
-#define ASPIS_MWS_H(TT, FF)                              \
-    switch (plan.sweeps) {                               \
-    case 16: ASPIS_MWS(TT, 16, true, FF) break;          \
-    case 24: ASPIS_MWS(TT, 24, true, FF) break;          \
-    case 32: ASPIS_MWS(TT, 32, true, FF) break;          \
-    default: return hipErrorInvalidValue;                \
-    }
-        if (plan.half && plan.fill == kWsFillWide) {
-            switch (T) {
-            case 64: ASPIS_MWS_H(64, kWsFillWide) break;
-            case 32: ASPIS_MWS_H(32, kWsFillWide) break;
-            default: return hipErrorInvalidValue;
-            }
-        } else if (plan.half) {
-            switch (T) {
-            case 128:
-                switch (plan.sweeps) {
-                case 8: ASPIS_MWS(128, 8, true, kWsFill) break;
-                case 16: ASPIS_MWS(128, 16, true, kWsFill) break;
-                case 24: ASPIS_MWS(128, 24, true, kWsFill) break;
-                case 26: ASPIS_MWS(128, 26, true, kWsFill) break;
-                case 28: ASPIS_MWS(128, 28, true, kWsFill) break;
-                case 30: ASPIS_MWS(128, 30, true, kWsFill) break;
-                case 32: ASPIS_MWS(128, 32, true, kWsFill) break;
-                default: return hipErrorInvalidValue;
-                }
-                break;
-            case 64: ASPIS_MWS_H(64, kWsFill) break;
-            case 32:
-                if (plan.sweeps == 36) {
-                    ASPIS_MWS(32, 36, true, kWsFill)
-                } else {
-                    ASPIS_MWS_H(32, kWsFill)
-                }
-                break;
-            case 16: ASPIS_MWS_H(16, kWsFill) break;
-            default: return hipErrorInvalidValue;
-            }
-        } else {
-            switch (T) {
-            case 64:
-                if (plan.sweeps == 16) {
-                    ASPIS_MWS(64, 16, false, kWsFill)
-                } else {
-                    ASPIS_MWS_T(64)
-                }
-                break;
-            case 32: ASPIS_MWS_T(32) break;
-            case 16: ASPIS_MWS_T(16) break;
-            case 8: ASPIS_MWS_T(8) break;
-            default: return hipErrorInvalidValue;
-            }
-        }
-#undef ASPIS_MWS_H
-#undef ASPIS_MWS_T
-#undef ASPIS_MWS
-        return hipGetLastError();
-    }
-    const int T = pick_tile(f, 0);
-    if (use) *use = TileUse{T, 0};
-    if (T == 0) return hipErrorInvalidValue;
-    const int64_t ntiles = (d + T - 1) / T;
-    const size_t lds = (size_t)(f * 4 * T + hist_words(T) * 4);
-    const unsigned grid = (unsigned)tile_grid(ntiles, lds);
-    const bool vec = (d % 4 == 0) && aligned16(g);
-#define ASPIS_MED(TT)                                                                        \
-    if (vec)                                                                                 \
-        median_kernel<TT, true><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
-                                                                   ntiles, out);             \
-    else                                                                                     \
-        median_kernel<TT, false><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
-                                                                    ntiles, out);
-    switch (T) {
-    case 64: ASPIS_MED(64) break;
-    case 32: ASPIS_MED(32) break;
-    case 16: ASPIS_MED(16) break;
-    case 8: ASPIS_MED(8) break;
-    case 4: ASPIS_MED(4) break;
-    default: return hipErrorInvalidValue;
-    }
-#undef ASPIS_MED
-    return hipGetLastError();
-}
-
 // LDS of the warp-specialised single pass: histograms, key tile, per-file
-// words (half keys: two nibbles per file) and, with a row table, the table.
-int64_t ws_lds_bytes(int64_t f, int r, int T, bool ind, bool half, int fill) {
+// words (half keys: two nibbles per file) and, with a row table in LDS, the
+// table.
+int64_t ws_lds_bytes(int64_t f, int r, int T, bool table_in_lds, bool half, int fill) {
     const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T, fill) + 2 * ((f + 7) / 8)
                                : hist_words(T) + f * (int64_t)T + 2 * f;
-    return words * 4 + (ind ? f * r * 4 : 0);
+    return words * 4 + (table_in_lds ? f * r * 4 : 0);
 }
 
 // Warp-specialised single pass (r = 3, 16-byte aligned rows): plans as for
-// the median above (the wide split without a row table).
+// the median above (the wide split without a row table in LDS).
 WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     WsPlan p;
     if (r != 3 || !vec) return p;
@@ -1982,19 +1977,248 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
         // a wider tile when the row table, read from global memory (where it
         // stays cached), leaves LDS to the keys: 2,300 files take 32 columns
         // instead of 16
-        WsPlan wide = half_plan(f, best.T, true, true, [&](int T, int fill) {
+        const WsPlan wide = half_plan(f, best.T, true, true, [&](int T, int fill) {
             return ws_lds_bytes(f, r, T, false, true, fill);
         });
-        if (wide.T != 0) {
-            wide.rtg = true;
-            best = wide;
-        }
+        if (wide.T != 0) best = wide;
     }
     return best;
 }
 
+// ---------------------------------------------------------------------------
+// The kernels built for each plan.  A launcher looks its kernel up here; a
+// plan with no entry is a planning error (reported by aspis_plan and the
+// launchers alike, never launched).
+
+using FusedWsFn = void (*)(const float *, const int32_t *, int64_t, int64_t, const int32_t *,
+                           const int32_t *, const int32_t *, int64_t, uint32_t *, float *);
+using MedianWsFn = void (*)(const float *, int64_t, const int32_t *, const int32_t *, int64_t,
+                            float *);
+
+FusedWsFn fused_ws_fn(const WsPlan &p, bool ind) {
+    const int key = p.T * 1000 + p.sweeps * 10 + (p.half ? 1 : 0);
+#define ASPIS_KEY(TT, SWW, HH) TT * 1000 + SWW * 10 + (HH ? 1 : 0)
+    // file-major, or with the row table in LDS
+#define ASPIS_FWS(TT, SWW, HH)                                                  \
+    case ASPIS_KEY(TT, SWW, HH):                                                \
+        return ind ? &fused_ws_kernel<TT, 3, SWW, true, HH, kWsFill, false>     \
+                   : &fused_ws_kernel<TT, 3, SWW, false, HH, kWsFill, false>;
+    if (p.rtg) {
+        // row table read from global memory: wide split, half keys
+        if (!ind || !p.half || p.fill != kWsFillWide) return nullptr;
+        switch (key) {
+#define ASPIS_FWS_RTG(TT, SWW)  \
+    case ASPIS_KEY(TT, SWW, true): return &fused_ws_kernel<TT, 3, SWW, true, true, kWsFillWide, true>;
+            ASPIS_FWS_RTG(64, 24)
+            ASPIS_FWS_RTG(64, 32)
+            ASPIS_FWS_RTG(32, 24)
+            ASPIS_FWS_RTG(32, 32)
+#undef ASPIS_FWS_RTG
+        default: return nullptr;
+        }
+    }
+    if (p.fill == kWsFillWide) {
+        // wide split: half keys, file-major only
+        if (ind || !p.half) return nullptr;
+        switch (key) {
+#define ASPIS_FWS_WIDE(TT, SWW) \
+    case ASPIS_KEY(TT, SWW, true): return &fused_ws_kernel<TT, 3, SWW, false, true, kWsFillWide, false>;
+            ASPIS_FWS_WIDE(64, 24)
+            ASPIS_FWS_WIDE(64, 32)
+            ASPIS_FWS_WIDE(32, 24)
+            ASPIS_FWS_WIDE(32, 32)
+#undef ASPIS_FWS_WIDE
+        default: return nullptr;
+        }
+    }
+    if (p.fill != kWsFill) return nullptr;
+    if (p.half && p.T == 32 && p.sweeps == 36)   // no room for a row table in LDS
+        return ind ? nullptr : &fused_ws_kernel<32, 3, 36, false, true, kWsFill, false>;
+    switch (key) {
+#define ASPIS_FWS_FULL(TT)    \
+    ASPIS_FWS(TT, 2, false)   \
+    ASPIS_FWS(TT, 4, false)   \
+    ASPIS_FWS(TT, 8, false)   \
+    ASPIS_FWS(TT, 12, false)  \
+    ASPIS_FWS(TT, 16, false)
+#define ASPIS_FWS_HALF(TT)    \
+    ASPIS_FWS(TT, 16, true)   \
+    ASPIS_FWS(TT, 24, true)   \
+    ASPIS_FWS(TT, 32, true)
+        ASPIS_FWS_FULL(64)
+        ASPIS_FWS_FULL(32)
+        ASPIS_FWS_FULL(16)
+        ASPIS_FWS_FULL(8)
+        ASPIS_FWS(128, 8, true)
+        ASPIS_FWS(128, 16, true)
+        ASPIS_FWS(128, 24, true)
+        ASPIS_FWS(128, 26, true)
+        ASPIS_FWS(128, 28, true)
+        ASPIS_FWS(128, 30, true)
+        ASPIS_FWS(128, 32, true)
+        ASPIS_FWS_HALF(64)
+        ASPIS_FWS_HALF(32)
+        ASPIS_FWS_HALF(16)
+#undef ASPIS_FWS_HALF
+#undef ASPIS_FWS_FULL
+    default: return nullptr;
+    }
+#undef ASPIS_FWS
+}
+
+MedianWsFn median_ws_fn(const WsPlan &p) {
+    const int key = p.T * 1000 + p.sweeps * 10 + (p.half ? 1 : 0);
+#define ASPIS_MWS(TT, SWW, HH, FF) \
+    case ASPIS_KEY(TT, SWW, HH): return &median_ws_kernel<TT, SWW, HH, FF>;
+    if (p.fill == kWsFillWide) {
+        if (!p.half) return nullptr;
+        switch (key) {
+            ASPIS_MWS(64, 16, true, kWsFillWide)
+            ASPIS_MWS(64, 24, true, kWsFillWide)
+            ASPIS_MWS(64, 32, true, kWsFillWide)
+            ASPIS_MWS(32, 16, true, kWsFillWide)
+            ASPIS_MWS(32, 24, true, kWsFillWide)
+            ASPIS_MWS(32, 32, true, kWsFillWide)
+        default: return nullptr;
+        }
+    }
+    if (p.fill != kWsFill) return nullptr;
+    switch (key) {
+#define ASPIS_MWS_FULL(TT)               \
+    ASPIS_MWS(TT, 4, false, kWsFill)     \
+    ASPIS_MWS(TT, 8, false, kWsFill)     \
+    ASPIS_MWS(TT, 12, false, kWsFill)
+#define ASPIS_MWS_HALF(TT)               \
+    ASPIS_MWS(TT, 16, true, kWsFill)     \
+    ASPIS_MWS(TT, 24, true, kWsFill)     \
+    ASPIS_MWS(TT, 32, true, kWsFill)
+        ASPIS_MWS_FULL(64)
+        ASPIS_MWS(64, 16, false, kWsFill)
+        ASPIS_MWS_FULL(32)
+        ASPIS_MWS_FULL(16)
+        ASPIS_MWS_FULL(8)
+        ASPIS_MWS(128, 8, true, kWsFill)
+        ASPIS_MWS(128, 16, true, kWsFill)
+        ASPIS_MWS(128, 24, true, kWsFill)
+        ASPIS_MWS(128, 26, true, kWsFill)
+        ASPIS_MWS(128, 28, true, kWsFill)
+        ASPIS_MWS(128, 30, true, kWsFill)
+        ASPIS_MWS(128, 32, true, kWsFill)
+        ASPIS_MWS_HALF(64)
+        ASPIS_MWS_HALF(32)
+        ASPIS_MWS(32, 36, true, kWsFill)
+        ASPIS_MWS_HALF(16)
+#undef ASPIS_MWS_HALF
+#undef ASPIS_MWS_FULL
+    default: return nullptr;
+    }
+#undef ASPIS_MWS
+#undef ASPIS_KEY
+}
+
+KernelPlan ws_kernel_plan(int kind, const WsPlan &p, int64_t lds, int table) {
+    KernelPlan k;
+    k.kind = kind;
+    k.tile_cols = p.T;
+    k.sweeps = p.sweeps;
+    k.half_keys = p.half ? 1 : 0;
+    k.stream_threads = p.fill;
+    k.row_table = table;
+    k.lds_bytes = lds;
+    k.block = kWsThreads;
+    return k;
+}
+
+}  // namespace
+
+bool plan_median(int64_t f, bool vec, KernelPlan *out) {
+    const WsPlan p = mws_plan(f, vec);
+    if (p.T != 0) {
+        *out = ws_kernel_plan(median_ws_fn(p) ? kKernelMedianWs : kKernelUnbuilt, p,
+                              mws_lds_bytes(f, p.T, p.half, p.fill), 0);
+        return out->kind == kKernelMedianWs;
+    }
+    KernelPlan k;
+    const int T = pick_tile(f, 0);
+    if (T != 0) {
+        k.kind = kKernelMedianTile;
+        k.tile_cols = T;
+        k.lds_bytes = f * 4 * T + hist_words(T) * 4;
+        k.block = (T >= 16 ? 1024 : 64 * T);
+    } else {
+        k.kind = kKernelMedianRadix;
+        k.tile_cols = kRadixCols;
+        k.lds_bytes = 0;   // static
+        k.block = kRadixThreads;
+    }
+    *out = k;
+    return true;
+}
+
+bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out) {
+    *out = KernelPlan{};
+    const WsPlan p = ws_plan(f, r, vec, ind);
+    if (p.T != 0) {
+        const int table = ind ? (p.rtg ? 2 : 1) : 0;
+        *out = ws_kernel_plan(fused_ws_fn(p, ind) ? kKernelFusedWs : kKernelUnbuilt, p,
+                              ws_lds_bytes(f, r, p.T, ind && !p.rtg, p.half, p.fill), table);
+        return out->kind == kKernelFusedWs;
+    }
+    if (r != 3 && r != 5 && r != 7) return false;
+    const int T = pick_tile(f, f * 4);
+    if (T == 0) return false;
+    out->kind = kKernelFused;
+    out->tile_cols = T;
+    out->row_table = ind ? 2 : 0;
+    out->lds_bytes = f * 4 * T + f * 4 + hist_words(T) * 4;
+    out->block = (T >= 16 ? 1024 : 64 * T);
+    return true;
+}
+
 bool fused_supported(int64_t f, int r) {
-    return (r == 3 || r == 5 || r == 7) && pick_tile(f, f * 4) != 0;
+    KernelPlan k;
+    return plan_fused(f, r, true, false, &k) || plan_fused(f, r, false, false, &k);
+}
+
+hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
+                         float *out, hipStream_t s, TileUse *use) {
+    const bool vec = (d % 4 == 0) && aligned16(g);
+    KernelPlan k;
+    if (!plan_median(f, vec, &k)) return hipErrorInvalidValue;
+    if (use) *use = TileUse{k.tile_cols, k.half_keys};
+    const int T = k.tile_cols;
+    const int64_t ntiles = (d + T - 1) / T;
+    if (k.kind == kKernelMedianWs) {
+        const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
+        const MedianWsFn fn = median_ws_fn(mws_plan(f, vec));
+        fn<<<grid, kWsThreads, (size_t)k.lds_bytes, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+        return hipGetLastError();
+    }
+    if (k.kind == kKernelMedianRadix) {
+        // LDS: 66 KB of histograms, two workgroups per CU
+        const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus() * 2);
+        median_radix_kernel<<<grid, kRadixThreads, 0, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+        return hipGetLastError();
+    }
+    const size_t lds = (size_t)k.lds_bytes;
+    const unsigned grid = (unsigned)tile_grid(ntiles, lds);
+#define ASPIS_MED(TT)                                                                        \
+    if (vec)                                                                                 \
+        median_kernel<TT, true><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
+                                                                   ntiles, out);             \
+    else                                                                                     \
+        median_kernel<TT, false><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
+                                                                    ntiles, out);
+    switch (T) {
+    case 64: ASPIS_MED(64) break;
+    case 32: ASPIS_MED(32) break;
+    case 16: ASPIS_MED(16) break;
+    case 8: ASPIS_MED(8) break;
+    case 4: ASPIS_MED(4) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_MED
+    return hipGetLastError();
 }
 
 hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
@@ -2002,112 +2226,19 @@ hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r,
                         TileUse *use) {
     const bool vec = (d % 4 == 0) && aligned16(g);
     const bool ind = row_of != nullptr;
-    const WsPlan plan = ws_plan(f, r, vec, ind);
-    if (use) *use = TileUse{plan.T, plan.half ? 1 : 0};
-    if (plan.T != 0) {
-        const int T = plan.T;
-        const int64_t ntiles = (d + T - 1) / T;
-        const size_t lds = (size_t)ws_lds_bytes(f, r, T, ind && !plan.rtg, plan.half, plan.fill);
+    KernelPlan k;
+    if (!plan_fused(f, r, vec, ind, &k)) return hipErrorInvalidValue;
+    if (use) *use = TileUse{k.tile_cols, k.half_keys};
+    const int T = k.tile_cols;
+    const int64_t ntiles = (d + T - 1) / T;
+    const size_t lds = (size_t)k.lds_bytes;
+    if (k.kind == kKernelFusedWs) {
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-#define ASPIS_WS1(TT, SWW, II, HH, FF)                                                           \
-    fused_ws_kernel<TT, 3, SWW, II, HH, FF><<<grid, kWsThreads, lds, s>>>(                        \
-        g, II ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
-#define ASPIS_WS_G(TT, SWW, FF)                                                                  \
-    fused_ws_kernel<TT, 3, SWW, true, true, FF, true><<<grid, kWsThreads, lds, s>>>(             \
-        g, row_of, f, d, ws.sel, ws.pos, ws.n_sel, ntiles, pair_diff, out);
-#define ASPIS_WS(TT, SWW, HH)                         \
-    if (ind) {                                        \
-        ASPIS_WS1(TT, SWW, true, HH, kWsFill)         \
-    } else {                                          \
-        ASPIS_WS1(TT, SWW, false, HH, kWsFill)        \
-    }
-#define ASPIS_WS_T(TT)                             \
-    switch (plan.sweeps) {                         \
-    case 2: ASPIS_WS(TT, 2, false) break;          \
-    case 4: ASPIS_WS(TT, 4, false) break;          \
-    case 8: ASPIS_WS(TT, 8, false) break;          \
-    case 12: ASPIS_WS(TT, 12, false) break;        \
-    case 16: ASPIS_WS(TT, 16, false) break;        \
-    default: return hipErrorInvalidValue;          \
-    }
-#define ASPIS_WS_H(TT)                             \
-    switch (plan.sweeps) {                         \
-    case 16: ASPIS_WS(TT, 16, true) break;         \
-    case 24: ASPIS_WS(TT, 24, true) break;         \
-    case 32: ASPIS_WS(TT, 32, true) break;         \
-    default: return hipErrorInvalidValue;          \
-    }
-#define ASPIS_WS_W(TT)                                              \
-    switch (plan.sweeps) {                                          \
-    case 24: ASPIS_WS1(TT, 24, false, true, kWsFillWide) break;     \
-    case 32: ASPIS_WS1(TT, 32, false, true, kWsFillWide) break;     \
-    default: return hipErrorInvalidValue;                           \
-    }
-        if (plan.rtg) {
-            if (!plan.half) return hipErrorInvalidValue;
-            switch (T * 100 + plan.sweeps + (plan.fill == kWsFillWide ? 10000 : 0)) {
-            case 16424: ASPIS_WS_G(64, 24, kWsFillWide) break;
-            case 16432: ASPIS_WS_G(64, 32, kWsFillWide) break;
-            case 13224: ASPIS_WS_G(32, 24, kWsFillWide) break;
-            case 13232: ASPIS_WS_G(32, 32, kWsFillWide) break;
-            default: return hipErrorInvalidValue;
-            }
-        } else if (plan.half && plan.fill == kWsFillWide) {
-            if (ind) return hipErrorInvalidValue;
-            switch (T) {
-            case 64: ASPIS_WS_W(64) break;
-            case 32: ASPIS_WS_W(32) break;
-            default: return hipErrorInvalidValue;
-            }
-        } else if (plan.half) {
-            switch (T) {
-            case 128:
-                switch (plan.sweeps) {
-                case 8: ASPIS_WS(128, 8, true) break;
-                case 16: ASPIS_WS(128, 16, true) break;
-                case 24: ASPIS_WS(128, 24, true) break;
-                case 26: ASPIS_WS(128, 26, true) break;
-                case 28: ASPIS_WS(128, 28, true) break;
-                case 30: ASPIS_WS(128, 30, true) break;
-                case 32: ASPIS_WS(128, 32, true) break;
-                default: return hipErrorInvalidValue;
-                }
-                break;
-            case 64: ASPIS_WS_H(64) break;
-            case 32:
-                if (plan.sweeps == 36) {
-                    // a row table in LDS leaves no room for this tile
-                    if (ind) return hipErrorInvalidValue;
-                    ASPIS_WS1(32, 36, false, true, kWsFill)
-                } else {
-                    ASPIS_WS_H(32)
-                }
-                break;
-            case 16: ASPIS_WS_H(16) break;
-            default: return hipErrorInvalidValue;
-            }
-        } else {
-            switch (T) {
-            case 64: ASPIS_WS_T(64) break;
-            case 32: ASPIS_WS_T(32) break;
-            case 16: ASPIS_WS_T(16) break;
-            case 8: ASPIS_WS_T(8) break;
-            default: return hipErrorInvalidValue;
-            }
-        }
-#undef ASPIS_WS_G
-#undef ASPIS_WS_W
-#undef ASPIS_WS_H
-#undef ASPIS_WS_T
-#undef ASPIS_WS
-#undef ASPIS_WS1
+        const FusedWsFn fn = fused_ws_fn(ws_plan(f, r, vec, ind), ind);
+        fn<<<grid, kWsThreads, lds, s>>>(g, ind ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel,
+                                         ntiles, pair_diff, out);
         return hipGetLastError();
     }
-    const int T = pick_tile(f, f * 4);
-    if (use) *use = TileUse{T, 0};
-    if (T == 0) return hipErrorInvalidValue;
-    const int64_t ntiles = (d + T - 1) / T;
-    const size_t lds = (size_t)(f * 4 * T + f * 4 + hist_words(T) * 4);
     const unsigned grid = (unsigned)tile_grid(ntiles, lds);
 #define ASPIS_FUSED(TT, RR)                                                                  \
     if (vec)                                                                                 \

@@ -1,12 +1,12 @@
 """Shared helpers of the GPU parity tests (not collected by pytest)."""
 from __future__ import annotations
 
-import concurrent.futures as cf
 import os
 
 import numpy as np
 
 import oracle
+from oracle import parallel as oracle_parallel
 
 WORKERS = min(16, os.cpu_count() or 1)
 
@@ -62,10 +62,4 @@ def assert_same_floats(got: np.ndarray, ref: np.ndarray, nan_equal: bool = False
 
 def threaded_agreement(chunk: np.ndarray) -> np.ndarray:
     """Oracle Eq. (4) over a [f, r, n] chunk, files split over threads."""
-    f = chunk.shape[0]
-    bounds = np.linspace(0, f, WORKERS + 1).astype(int)
-    with cf.ThreadPoolExecutor(WORKERS) as ex:
-        parts = list(ex.map(lambda b: oracle.pair_agreement(chunk[b[0]:b[1]]),
-                            [(bounds[t], bounds[t + 1]) for t in range(WORKERS)
-                             if bounds[t + 1] > bounds[t]]))
-    return np.concatenate(parts, axis=0)
+    return oracle_parallel.agreement(chunk, WORKERS)

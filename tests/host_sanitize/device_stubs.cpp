@@ -32,7 +32,15 @@ hipError_t launch_select(const int32_t *, const int8_t *, int64_t, int, int, uin
                          hipStream_t) {
     return hipErrorInvalidValue;
 }
-int pick_median_tile(int64_t f) { return f <= 1000 ? 64 : 0; }
+bool plan_median(int64_t, bool, KernelPlan *out) {
+    *out = KernelPlan{};
+    out->kind = kKernelMedianRadix;
+    return true;
+}
+bool plan_fused(int64_t, int, bool, bool, KernelPlan *out) {
+    *out = KernelPlan{};
+    return false;
+}
 hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, float *, hipStream_t,
                          TileUse *) {
     return hipErrorInvalidValue;

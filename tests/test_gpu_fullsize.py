@@ -1,9 +1,16 @@
 """GPU parity at the workloads' full sizes, in the launch configuration the
-benchmark times (the single-pass path).  The replica tensor is written on the
-GPU by the generator; every coordinate is regenerated on the host and
-compared byte for byte with what the GPU consumed, the oracle's agreement
-runs over every coordinate, and the oracle's median is computed for a
-seeded sample of coordinates (plus the first and last)."""
+benchmark times (the single-pass path), on every coordinate.
+
+The replica tensor is written on the GPU by the generator.  Pass 1 walks
+the coordinates in chunks of about 1 GiB of replicas: each chunk is
+regenerated on the host and compared byte for byte with what the GPU holds,
+and the oracle's agreement (Eq. 4) runs on it.  The oracle then detects,
+votes and selects (Algorithm 3, Algorithm 1) on the whole-vector agreement.
+Pass 2 reads every chunk back (bytes pass 1 proved equal to the host
+generator's, which the library only reads) and compares the oracle's median
+of the kept replicas with the GPU's output, coordinate by coordinate.  The
+oracle runs chunk-parallel over host threads (oracle.parallel), which splits
+coordinates or files only."""
 import time
 
 import numpy as np
@@ -11,19 +18,24 @@ import pytest
 
 import oracle
 import synth
+from oracle import parallel as oracle_parallel
 from paper_2108_02416_amd import aspis
 
-from _helpers import (WORKERS, assert_detection, assert_same_floats, device, threaded_agreement,
-                      to_np)
+from _helpers import WORKERS, assert_detection, assert_same_floats, device, to_np
 
 pytestmark = pytest.mark.gpu
 
 CHUNK_BYTES = 1 << 30
-N_SAMPLE = 1024
 
 
 def _log(msg):
     print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def _chunks(f, r, d):
+    step = max(1024, CHUNK_BYTES // (f * r * 4))
+    for k0 in range(0, d, step):
+        yield k0, min(step, d - k0)
 
 
 @pytest.mark.parametrize("idx,seed", [(1, synth.SEED), (2, synth.SEED), (3, synth.SEED),
@@ -37,6 +49,7 @@ def test_fullsize_workload(idx, seed):
     s = oracle.assign(K, r)
     role, worker, A, D = synth.make_roles(wl, s, seed)
     _log(f"workload {idx} seed {seed}: {wl.name} f={f} ({wl.replica_bytes() / 1e9:.2f} GB) A={A}")
+    t0 = time.perf_counter()
     gd = torch.empty((f, r, d), dtype=torch.float32, device=device())
     synth.fill_device(role, worker, gd, wl.dist, seed=seed, alie_z=wl.alie_z)
     got = aspis.detect_aggregate(gd, K, r, q, flags=aspis.FLAG_TIMING)
@@ -44,34 +57,36 @@ def test_fullsize_workload(idx, seed):
     _log(f"gpu done: {got['stats']}")
     assert got["stats"]["fused"] == 1
 
-    rng = np.random.default_rng(428 + idx)
-    sample = np.unique(np.concatenate([[0, d - 1], rng.integers(0, d, N_SAMPLE)]))
-    cols = np.empty((f, r, sample.size), dtype=np.float32)
+    # pass 1: input bytes and the oracle's agreement over every coordinate
     alpha = np.ones((f, r * (r - 1) // 2), dtype=np.uint8)
-    step = max(1024, CHUNK_BYTES // (f * r * 4))
-    host = np.empty((f, r, step), dtype=np.float32)
-    for k0 in range(0, d, step):
-        n = min(step, d - k0)
-        h = host[:, :, :n] if n == step else np.empty((f, r, n), dtype=np.float32)
-        synth.fill(role, worker, k0, n, wl.dist, seed, alie_z=wl.alie_z, out=h,
+    host = None
+    for k0, n in _chunks(f, r, d):
+        if host is None or host.shape[2] != n:
+            host = np.empty((f, r, n), dtype=np.float32)
+        synth.fill(role, worker, k0, n, wl.dist, seed, alie_z=wl.alie_z, out=host,
                    nthreads=WORKERS)
         dev = gd[:, :, k0:k0 + n].contiguous().cpu().numpy()
-        assert np.array_equal(dev.view(np.uint32), h.view(np.uint32)), \
+        assert np.array_equal(dev.view(np.uint32), host.view(np.uint32)), \
             f"GPU input differs from the host generator in coordinates [{k0}, {k0 + n})"
-        alpha &= threaded_agreement(h)
-        inside = (sample >= k0) & (sample < k0 + n)
-        cols[:, :, inside] = h[:, :, sample[inside] - k0]
-    _log("host regeneration + oracle agreement done")
+        alpha &= oracle_parallel.agreement(host, WORKERS)
+    t1 = time.perf_counter()
+    _log(f"pass 1 (regeneration, byte compare, agreement): {t1 - t0:.1f} s")
 
     ref = oracle.detect(None, s, K, q, alpha=alpha)
     assert_detection(got, ref, K)
     cl = ref["clique"]
     sel, kept = oracle.select(s, ref["vote"], cl["success"], cl["honest"])
     assert (to_np(got["sel"]) == sel).all() and got["n_selected"] == kept
-    med = oracle.median(cols, sel)
-    assert_same_floats(to_np(got["out"])[sample], med)
-    _log(f"detection, selection and {sample.size} sampled medians match "
-         f"(omega={cl['omega']}, max cliques={cl['n_maximum']}, success={cl['success']})")
+
+    # pass 2: the oracle's median over every coordinate
+    out = to_np(got["out"])
+    for k0, n in _chunks(f, r, d):
+        dev = gd[:, :, k0:k0 + n].contiguous().cpu().numpy()
+        med = oracle_parallel.median_by_coordinates(dev, sel, WORKERS)
+        assert_same_floats(out[k0:k0 + n], med)
+    _log(f"pass 2 (median of {kept} kept replicas at all {d} coordinates): "
+         f"{time.perf_counter() - t1:.1f} s; omega={cl['omega']}, "
+         f"max cliques={cl['n_maximum']}, success={cl['success']}")
     del gd
     torch.cuda.empty_cache()
 
