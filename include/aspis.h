@@ -202,6 +202,32 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
                                     size_t ws_bytes, uint32_t flags,
                                     aspis_run_stats *stats, void *stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, serving
+ * loops and harnesses that forbid hipMalloc): aspis_detect_aggregate
+ * without a workspace argument.  Its scratch (the selection, the kept-row
+ * list, a counter and the staged disagreement rows) lives in a static
+ * device array of ASPIS_NOALLOC_SCRATCH_BYTES, one per device, held until
+ * the process ends; its address is looked up on the first call on each
+ * device.  The call allocates no device or host memory, and creates no
+ * events.  Nothing in the array needs to start at zero: every part is
+ * written before it is read.  Every call on one device shares that
+ * device's array, so calls that overlap on one device (other streams or
+ * threads) race and must be serialised by the caller.
+ * Same arguments, outputs and errors as aspis_detect_aggregate, plus
+ * BUFFER_SMALL when aspis_aggregate_workspace(K, r, d) exceeds the array
+ * (every K <= 64 at r = 3; K <= 25 at r = 5; K <= 19 at r = 7) and
+ * INVALID_ARG for
+ * ASPIS_FLAG_TIMING (which would create events). */
+#define ASPIS_NOALLOC_SCRATCH_BYTES ((size_t)2 << 20)
+aspis_status aspis_detect_aggregate_noalloc(const float *grads, int32_t K, int32_t r,
+                                            int32_t q, int64_t d,
+                                            const int32_t *subsets_dev,
+                                            const aspis_detect_out *det,
+                                            aspis_reduce mode, float *out,
+                                            int32_t *sel_out, aspis_clique_result *res,
+                                            int64_t *n_selected, uint32_t flags,
+                                            aspis_run_stats *stats, void *stream);
+
 /* The worker-major upload of Algorithm 1: worker u returns the gradients
  * of its l = C(K-1,r-1) files in ascending file order, one after another,
  * so the upload of all K workers is a float32 [K][l][d] tensor.  Writes, for

@@ -26,7 +26,8 @@ FLAG_TIMING = 2
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
     "aspis_aggregate_workspace", "aspis_aggregate", "aspis_detect_aggregate",
-    "aspis_detect_aggregate_wm", "aspis_worker_rows", "aspis_plan",
+    "aspis_detect_aggregate_wm", "aspis_detect_aggregate_noalloc", "aspis_worker_rows",
+    "aspis_plan",
     "aspis_read_probe_sink_words", "aspis_read_probe", "aspis_simulate", "aspis_detox",
     "aspis_last_error",
 )
@@ -138,6 +139,12 @@ def lib():
     L.aspis_detect_aggregate.restype = ctypes.c_int
     L.aspis_detect_aggregate_wm.argtypes = L.aspis_detect_aggregate.argtypes
     L.aspis_detect_aggregate_wm.restype = ctypes.c_int
+    L.aspis_detect_aggregate_noalloc.argtypes = [P, i32, i32, i32, i64, P,
+                                                 ctypes.POINTER(DetectOut), ctypes.c_int, P, P,
+                                                 ctypes.POINTER(CliqueResult),
+                                                 ctypes.POINTER(i64), u32,
+                                                 ctypes.POINTER(RunStats), P]
+    L.aspis_detect_aggregate_noalloc.restype = ctypes.c_int
     L.aspis_worker_rows.argtypes = [i32, i32, P, i64]
     L.aspis_worker_rows.restype = ctypes.c_int
     L.aspis_plan.argtypes = [i32, i32, i64, i32, ctypes.POINTER(KernelPlan),
@@ -400,6 +407,27 @@ def detect_aggregate(grads, K: int, r: int, q: int, mode: str = "median", flags:
         ctypes.byref(det), REDUCE[mode], out.data_ptr(),
         sel_out.data_ptr() if sel_out is not None else None, ctypes.byref(res),
         ctypes.byref(n_sel), wp, wn, flags, ctypes.byref(stats), _stream_ptr())
+    _check(st)
+    return {"out": out, "sel": sel_out, "bufs": bufs, "clique": res,
+            "n_selected": int(n_sel.value), "stats": stats.as_dict()}
+
+
+def detect_aggregate_noalloc(grads, K: int, r: int, q: int, bufs: DetectBuffers, out,
+                             sel_out=None, mode: str = "median", flags: int = 0) -> dict:
+    """aspis_detect_aggregate_noalloc: the whole step with the library's
+    static device scratch instead of a workspace; the caller passes every
+    output buffer (nothing is allocated here either)."""
+    f, d = _check_grads(grads, K, r)
+    _check_outputs(grads.device, f, K, d, bufs=bufs, out=out, sel_out=sel_out)
+    res = CliqueResult()
+    stats = RunStats()
+    n_sel = ctypes.c_int64(0)
+    det = bufs.c()
+    st = lib().aspis_detect_aggregate_noalloc(
+        grads.data_ptr(), K, r, q, d, subsets_device(K, r, grads.device).data_ptr(),
+        ctypes.byref(det), REDUCE[mode], out.data_ptr(),
+        sel_out.data_ptr() if sel_out is not None else None, ctypes.byref(res),
+        ctypes.byref(n_sel), flags, ctypes.byref(stats), _stream_ptr())
     _check(st)
     return {"out": out, "sel": sel_out, "bufs": bufs, "clique": res,
             "n_selected": int(n_sel.value), "stats": stats.as_dict()}

@@ -368,12 +368,12 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     hipEvent_t *ev = events.e;
     if (timing)
         for (int i = 0; i < 6; ++i) ASPIS_HIP(hipEventCreate(&ev[i]));
-    std::vector<uint64_t> rows(K);
+    uint64_t rows[ASPIS_MAX_K_DEVICE];
     auto graph_to_host = [&](aspis_clique_result *out_res) -> aspis_status {
-        ASPIS_HIP(hipMemcpyAsync(rows.data(), det->disagree, sizeof(uint64_t) * K,
+        ASPIS_HIP(hipMemcpyAsync(rows, det->disagree, sizeof(uint64_t) * K,
                                  hipMemcpyDeviceToHost, s));
         ASPIS_HIP(hipStreamSynchronize(s));
-        return aspis_clique(rows.data(), K, q, out_res);
+        return aspis_clique(rows, K, q, out_res);
     };
     aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
     // the row of every replica in a worker-major upload, in the workspace.
@@ -530,6 +530,33 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r, in
                                  res, n_selected, workspace, ws_bytes, flags, stats, stream);
 }
 
+aspis_status aspis_detect_aggregate_noalloc(const float *grads, int32_t K, int32_t r, int32_t q,
+                                            int64_t d, const int32_t *subsets_dev,
+                                            const aspis_detect_out *det, aspis_reduce mode,
+                                            float *out, int32_t *sel_out,
+                                            aspis_clique_result *res, int64_t *n_selected,
+                                            uint32_t flags, aspis_run_stats *stats,
+                                            void *stream) {
+    int64_t f = 0;
+    aspis_status st = check_device_shape(K, r, d, &f);
+    if (st != ASPIS_OK) return st;
+    if (flags & ASPIS_FLAG_TIMING)
+        return fail(ASPIS_ERR_INVALID_ARG,
+                    "aspis_detect_aggregate_noalloc: ASPIS_FLAG_TIMING creates timing events; "
+                    "not available here");
+    const size_t need = aspis::workspace_bytes(f, r);
+    if (need > aspis::kScratchBytes)
+        return fail(ASPIS_ERR_BUFFER_SMALL,
+                    "aspis_detect_aggregate_noalloc: K=%d r=%d needs %zu bytes of scratch, the "
+                    "static scratch holds %zu (use aspis_detect_aggregate with a workspace)",
+                    K, r, need, aspis::kScratchBytes);
+    void *scratch = nullptr;
+    ASPIS_HIP(aspis::scratch_ptr(&scratch));
+    return detect_aggregate_impl(grads, false, K, r, q, d, subsets_dev, det, mode, out, sel_out,
+                                 res, n_selected, scratch, aspis::kScratchBytes, flags, stats,
+                                 stream);
+}
+
 aspis_status aspis_detect_aggregate_wm(const float *grads_wm, int32_t K, int32_t r, int32_t q,
                                        int64_t d, const int32_t *subsets_dev,
                                        const aspis_detect_out *det, aspis_reduce mode, float *out,
@@ -552,6 +579,7 @@ aspis_status aspis_worker_rows(int32_t K, int32_t r, int32_t *row_of, int64_t ca
     return ASPIS_OK;
 }
 
+static_assert(ASPIS_NOALLOC_SCRATCH_BYTES == aspis::kScratchBytes, "scratch size of aspis.h");
 static_assert(ASPIS_KERNEL_NONE == aspis::kKernelNone && ASPIS_KERNEL_FUSED_WS == aspis::kKernelFusedWs &&
                   ASPIS_KERNEL_FUSED == aspis::kKernelFused &&
                   ASPIS_KERNEL_MEDIAN_WS == aspis::kKernelMedianWs &&

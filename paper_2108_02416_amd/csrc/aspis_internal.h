@@ -123,6 +123,12 @@ hipError_t launch_fused_mean(const float *g, const int32_t *row_of, int64_t f, i
                              hipStream_t s);
 bool fused_mean_supported(int64_t f, int r);
 
+// Device address of this device's static scratch array (kScratchBytes,
+// 256-aligned), the workspace of the allocation-free entry point.  Looked
+// up on the first call per device (the calling thread's current device).
+constexpr size_t kScratchBytes = (size_t)2 << 20;
+hipError_t scratch_ptr(void **out);
+
 size_t read_probe_sink_words();
 hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink,
                              hipStream_t s);

@@ -2310,6 +2310,32 @@ hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws, float *ou
     return hipGetLastError();
 }
 
+// The workspace of the allocation-free entry point: a static device array,
+// one copy per device, whose device address is looked up once per device
+// with that device current (in host code the array's name is a host-side
+// stand-in, never a device address).
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+std::atomic<void *> g_scratch[kMaxDevices];
+}  // namespace
+
+hipError_t scratch_ptr(void **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return hipSuccess;
+}
+
 size_t read_probe_sink_words() { return (size_t)kProbeBlocks * kBlock; }
 
 hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink, hipStream_t s) {

@@ -58,6 +58,7 @@ hipError_t launch_fused_mean(const float *, const int32_t *, int64_t, int, int64
     return hipErrorInvalidValue;
 }
 bool fused_mean_supported(int64_t, int) { return false; }
+hipError_t scratch_ptr(void **) { return hipErrorInvalidValue; }
 size_t read_probe_sink_words() { return 0; }
 hipError_t launch_read_probe(const void *, size_t, uint32_t *, hipStream_t) {
     return hipErrorInvalidValue;
