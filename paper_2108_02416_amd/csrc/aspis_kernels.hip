@@ -1091,18 +1091,21 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     // key registers per sweep: 4 keys, or (HALF) 4 high halves packed in 2;
     // a half-key tile's rows are the files themselves
     constexpr int KW = HALF ? 2 : 4;
-    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T, FILL) && RPI % 8 == 0 && R <= 4),
+    static_assert(!HALF || (SW % 2 == 0 && RPI == half_rpi(T, FILL) && RPI % 8 == 0 && R <= 7),
                   "half-key sweeps");
+    // a file's pair-difference bits fit a nibble only at r = 3 (3 bits)
+    constexpr bool PDN = HALF && R == 3;
     const int n = *n_sel;
     const int64_t hwords = HALF ? half_hist_words(T) : hist_words(T);
     const int64_t f8 = (f + 7) / 8;
     uint32_t *hist = smem;               // selection histograms
     uint32_t *tile = smem + hwords;
     // per-file words.  Full keys: pd [f] pair-difference bits, ps [f]
-    // (tile row << 3) | slot or -1.  Half keys (tile row = file): one nibble
-    // per file, pd [f/8] pair-difference bits, ps [f/8] 8 | slot or 0
+    // (tile row << 3) | slot or -1.  Half keys (tile row = file): ps [f/8],
+    // one nibble per file, 8 | slot or 0; pd [f/8] pair-difference nibbles
+    // at r = 3, else pd [f] words
     uint32_t *pd = tile + (HALF ? half_tile_words(f, T, FILL) : f * T);
-    int32_t *ps = reinterpret_cast<int32_t *>(pd + (HALF ? f8 : f));
+    int32_t *ps = reinterpret_cast<int32_t *>(pd + (PDN ? f8 : f));
     // [f*R] row table (IND): staged in LDS, or (RTG) read from global
     // memory, where it stays cached, when LDS is needed for a wider tile
     int32_t *rt_lds = ps + (HALF ? f8 : f);
@@ -1115,9 +1118,9 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
                 const int64_t i = 8 * w + e;
                 if (i < f && pos[i] >= 0) v |= (8u | (uint32_t)sel[i]) << (4 * e);
             }
-            pd[w] = 0u;
             ps[w] = (int32_t)v;
         }
+        for (int64_t w = tid; w < (PDN ? f8 : f); w += kWsThreads) pd[w] = 0u;
     } else {
         for (int64_t i = tid; i < f; i += kWsThreads) {
             pd[i] = 0u;
@@ -1239,9 +1242,9 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
         };
         // sweep 0 of the next tile, loaded early: before the barrier and the
         // hand-over, so that loads stay in flight meanwhile.  The 36-sweep
-        // tile and the row-table reads have no registers to spare for it and
-        // load it with their tile
-        constexpr bool kEarly0 = SW <= 32 && !IND;
+        // tile, the row-table reads and r = 5 (five chunks a sweep) have no
+        // registers to spare for it and load it with their tile
+        constexpr bool kEarly0 = SW <= 32 && !IND && R == 3;
         Chunks c0;
         // tile t from its sweep 0 (already in c0, or loaded first); the
         // other sweeps go in bursts of B, all loads of a burst issued first
@@ -1305,7 +1308,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
             const int i = j0 + x * RPI;
             const uint32_t b = (pdacc[x / PER] >> (NPB * (x % PER))) & ((1u << NPB) - 1u);
             if (i < f && b) {
-                if constexpr (HALF)
+                if constexpr (PDN)
                     atomicOr(&pd[i >> 3], b << ((i & 7) * 4));
                 else
                     atomicOr(&pd[i], b);
@@ -1334,7 +1337,7 @@ fused_ws_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of,
     }
     __syncthreads();
     for (int64_t i = tid; i < f; i += kWsThreads) {
-        const uint32_t b = HALF ? ((pd[i >> 3] >> ((i & 7) * 4)) & 15u) : pd[i];
+        const uint32_t b = PDN ? ((pd[i >> 3] >> ((i & 7) * 4)) & 15u) : pd[i];
         if (b) atomicOr(&pair_diff[i], b);
     }
 }
@@ -1854,6 +1857,7 @@ namespace {
 // sweep, so that thousands of rows fit the registers of a 32- or 64-column
 // tile.
 struct WsPlan {
+    int r = 3;
     int T = 0;
     int sweeps = 0;
     bool half = false;
@@ -1878,7 +1882,12 @@ constexpr int max_half_sweeps(int T, int fill) { return T == 32 && fill == kWsFi
 // only for 128 columns, where fewer than 128 rows never take a narrower
 // half-key tile, and steps of 2 from 24 to 32 there; 36 for 32 columns
 // (even split); 24 or 32 for the wide split.
-int round_sweeps(int64_t sw, bool half, int T, int fill) {
+int round_sweeps(int64_t sw, bool half, int T, int fill, int r = 3) {
+    if (half && r != 3) {
+        // r = 5: the sweep counts built for five replicas a file
+        if (T == 128) return sw <= 16 ? 16 : sw <= 30 ? 30 : 32;
+        return sw <= 16 ? 16 : sw <= 24 ? 24 : 32;
+    }
     if (half) {
         if (fill == kWsFillWide) return sw <= 24 ? 24 : 32;
         if (T == 128 && sw > 24) return (int)((sw + 1) / 2 * 2);
@@ -1899,19 +1908,20 @@ int round_sweeps(int64_t sw, bool half, int T, int fill) {
 // table's addresses next to its keys (the kernels built for a global
 // table are wide-split ones).
 template <typename LdsFn>
-WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds) {
+WsPlan half_plan(int64_t f, int narrower, bool ind, bool rtg, LdsFn &&lds, int r = 3) {
     WsPlan p;
     if (f < kHalfMinRows || f > kHalfMaxRows) return p;
     for (int T : {128, 64, 32, 16}) {
         if (T <= narrower) break;
         for (int fill : {kWsFill, kWsFillWide}) {
-            if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16)) continue;
+            if (fill == kWsFillWide && ((ind && !rtg) || T == 128 || T == 16 || r != 3)) continue;
             if (rtg && fill != kWsFillWide) continue;
             const int64_t rpi = half_rpi(T, fill);
             const int64_t sw = (f + rpi - 1) / rpi;
-            if (sw > (ind ? 32 : max_half_sweeps(T, fill)) || lds(T, fill) > kLdsBytes) continue;
+            const int64_t max_sw = (ind || r != 3) ? 32 : max_half_sweeps(T, fill);
+            if (sw > max_sw || lds(T, fill) > kLdsBytes) continue;
             p.T = T;
-            p.sweeps = round_sweeps(sw, true, T, fill);
+            p.sweeps = round_sweeps(sw, true, T, fill, r);
             p.half = true;
             p.fill = fill;
             p.rtg = rtg;
@@ -1950,16 +1960,29 @@ WsPlan mws_plan(int64_t f, bool vec) {
 // words (half keys: two nibbles per file) and, with a row table in LDS, the
 // table.
 int64_t ws_lds_bytes(int64_t f, int r, int T, bool table_in_lds, bool half, int fill) {
-    const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T, fill) + 2 * ((f + 7) / 8)
+    // half keys: slot nibbles, and pair-difference nibbles (r = 3) or words
+    const int64_t words = half ? half_hist_words(T) + half_tile_words(f, T, fill) + (f + 7) / 8 +
+                                     (r == 3 ? (f + 7) / 8 : f)
                                : hist_words(T) + f * (int64_t)T + 2 * f;
     return words * 4 + (table_in_lds ? f * r * 4 : 0);
 }
 
-// Warp-specialised single pass (r = 3, 16-byte aligned rows): plans as for
-// the median above (the wide split without a row table in LDS).
+// Warp-specialised single pass (16-byte aligned rows): plans as for the
+// median above (the wide split without a row table in LDS).  r = 5: half-key
+// tiles of the file-major tensor, even split (five 16-byte chunks a sweep
+// leave the streaming role no registers for more).
 WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
     WsPlan p;
-    if (r != 3 || !vec) return p;
+    if (!vec) return p;
+    if (r == 5 && !ind) {
+        p.r = 5;
+        WsPlan h = half_plan(f, 0, false, false, [&](int T, int fill) {
+            return ws_lds_bytes(f, r, T, false, true, fill);
+        }, 5);
+        h.r = 5;
+        return h.T != 0 ? h : WsPlan{};
+    }
+    if (r != 3) return p;
     for (int T : {64, 32, 16, 8}) {
         if (ws_lds_bytes(f, r, T, ind, false, kWsFill) > kLdsBytes) continue;
         const int64_t rpi = kWsFill / (T / 4);
@@ -1998,6 +2021,29 @@ using MedianWsFn = void (*)(const float *, int64_t, const int32_t *, const int32
 FusedWsFn fused_ws_fn(const WsPlan &p, bool ind) {
     const int key = p.T * 1000 + p.sweeps * 10 + (p.half ? 1 : 0);
 #define ASPIS_KEY(TT, SWW, HH) TT * 1000 + SWW * 10 + (HH ? 1 : 0)
+    if (p.r == 5) {
+        // five replicas a file: half keys, file-major, even split
+        if (ind || !p.half || p.fill != kWsFill || p.rtg) return nullptr;
+        switch (key) {
+#define ASPIS_FWS5(TT, SWW) \
+    case ASPIS_KEY(TT, SWW, true): return &fused_ws_kernel<TT, 5, SWW, false, true, kWsFill, false>;
+            ASPIS_FWS5(128, 16)
+            ASPIS_FWS5(128, 30)
+            ASPIS_FWS5(128, 32)
+            ASPIS_FWS5(64, 16)
+            ASPIS_FWS5(64, 24)
+            ASPIS_FWS5(64, 32)
+            ASPIS_FWS5(32, 16)
+            ASPIS_FWS5(32, 24)
+            ASPIS_FWS5(32, 32)
+            ASPIS_FWS5(16, 16)
+            ASPIS_FWS5(16, 24)
+            ASPIS_FWS5(16, 32)
+#undef ASPIS_FWS5
+        default: return nullptr;
+        }
+    }
+    if (p.r != 3) return nullptr;
     // file-major, or with the row table in LDS
 #define ASPIS_FWS(TT, SWW, HH)                                                  \
     case ASPIS_KEY(TT, SWW, HH):                                                \

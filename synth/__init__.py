@@ -7,7 +7,8 @@ which value (the attack simulation of Section 4.1 / 4.2 of the paper) and
 writes the numbers (``synth.hip``: a host fill for the oracle and a GPU fill
 that writes the same bytes straight into device memory).
 
-Workloads (shapes of the paper's CIFAR-10 / ResNet-18 experiments, r = 3):
+Workloads (shapes of the paper's CIFAR-10 / ResNet-18 experiments; r = 3
+except workload 6):
 
   1  K=7,  q=2, d=100,000     weak attack, workers {0,1}, reversed gradient
   2  K=15, q=3, d=1,000,000   weak attack, 3 seeded-random workers, ALIE
@@ -17,6 +18,8 @@ Workloads (shapes of the paper's CIFAR-10 / ResNet-18 experiments, r = 3):
                               colluders + 2 independent N(0,1) noise senders
   5  K=25, q=6, d=2,000,000   optimal attack, greedy choice, Student-t(3)
                               honest gradients, reversed gradient
+  6  K=11, r=5, q=4, d=6,500,000  optimal attack, exhaustive choice, ALIE:
+                              the redundancy r = 5 at 462 files
 """
 from __future__ import annotations
 
@@ -101,6 +104,8 @@ WORKLOADS = {
     3: Workload(3, 15, 3, 4, 11_200_000, DIST_NORMAL, "optimal", "alie", "exhaustive"),
     4: Workload(4, 21, 3, 5, 5_000_000, DIST_NORMAL, "weak", "alie+noise", "random"),
     5: Workload(5, 25, 3, 6, 2_000_000, DIST_STUDENT3, "optimal", "reversed", "greedy"),
+    # r = 5: five replicas a file, 462 files (the headline's file count), 60 GB
+    6: Workload(6, 11, 5, 4, 6_500_000, DIST_NORMAL, "optimal", "alie", "exhaustive"),
 }
 
 

@@ -90,6 +90,8 @@ CASES = [
     ("K=24 worker-major fused_ws<32,3,24,wide,table in HBM>", (24, 3, 5, "optimal", "reversed"),
      "worker", 0,
      dict(kernel="fused_ws", tile_cols=32, sweeps=24, stream_threads=768, row_table=2), 12),
+    ("K=11 r=5 fused_ws<128,5,30,half>", 6, "file", 0,
+     dict(kernel="fused_ws", tile_cols=128, sweeps=30, stream_threads=512), 36),
     ("headline two-pass median_ws<128,30,half>", 3, "file", _WS,
      dict(kernel="median_ws", tile_cols=128, sweeps=30), 36),
     ("K=25 two-pass median_ws<16,24,half>", 5, "file", _WS,
@@ -229,3 +231,27 @@ def test_median_beyond_lds_case2_ties():
     assert_detection(got, ref, K)
     assert (to_np(got["sel"]) == ref["sel"]).all()
     assert_same_floats(to_np(got["out"]), ref["out"])
+
+
+@pytest.mark.parametrize("K,q,attack", [(10, 3, "optimal"), (11, 4, "optimal"), (12, 3, "weak"),
+                                        (13, 5, "optimal"), (14, 4, "weak"), (15, 6, "optimal")])
+def test_r5_half_key_single_pass(K, q, attack):
+    """r = 5 in the warp-specialised single pass (252 to 3,003 files, 128- to
+    16-column half-key tiles): ten slot pairs a file, their bits kept in a
+    word per file; a few tiles and a ragged last one, weak and Theorem 1
+    attacks (ALIE)."""
+    r = 5
+    sp, _ = aspis.plan(K, r, 4096)
+    assert sp["kernel"] == "fused_ws" and sp["half_keys"] == 1, sp
+    T = sp["tile_cols"]
+    d = T * 9 + 12
+    wl = synth.Workload(0, K, r, q, d, synth.DIST_NORMAL, attack, "alie", "fixed")
+    s = oracle.assign(K, r)
+    g, _ = synth.generate(wl, s, d=d)
+    print(f"r=5 single pass: K={K} f={comb(K, r)} q={q} {attack} T={T} d={d}", flush=True)
+    for mode in ("median", "paper"):
+        got = _run(g, K, r, q, mode)
+        _compare(got, _oracle(g, K, r, q, mode), K, mode)
+        assert got["stats"]["fused"] == 1
+        if mode == "median":
+            assert got["stats"]["tile_cols"] == T and got["stats"]["half_keys"] == 1

@@ -84,6 +84,7 @@ CASES = {
     3: (11, 2, False, 455, 28, 28, 0),
     4: (16, 1, True, 1320, 55, 83, 115),
     5: (19, 2, False, 2300, 110, 110, 0),
+    6: (7, 2, False, 462, 28, 28, 0),      # r = 5: 1/2 C(8,5) = 28
 }
 
 

@@ -52,28 +52,34 @@ def test_overflowing_shapes_are_refused():
     assert e.value.status == aspis.ERR_OVERFLOW
 
 
-@pytest.mark.parametrize("K,layout,expect", [
+@pytest.mark.parametrize("K,layout,expect,r", [
     # the headline: 128-column half-key tiles, 30 sweeps
     (15, "file", dict(kernel="fused_ws", tile_cols=128, sweeps=30, half_keys=1,
-                      stream_threads=512, row_table=0)),
+                      stream_threads=512, row_table=0), 3),
     (15, "worker", dict(kernel="fused_ws", tile_cols=128, sweeps=30, half_keys=1,
-                        stream_threads=512, row_table=1)),
+                        stream_threads=512, row_table=1), 3),
     (21, "file", dict(kernel="fused_ws", tile_cols=32, sweeps=24, half_keys=1,
-                      stream_threads=512)),
+                      stream_threads=512), 3),
     (25, "file", dict(kernel="fused_ws", tile_cols=32, sweeps=36, half_keys=1,
-                      stream_threads=512)),
+                      stream_threads=512), 3),
     # a row table read from global memory takes the wide split (12
     # streaming waves): 2,024 and 2,300 files
     (24, "worker", dict(kernel="fused_ws", tile_cols=32, sweeps=24, half_keys=1,
-                        stream_threads=768, row_table=2)),
+                        stream_threads=768, row_table=2), 3),
     (25, "worker", dict(kernel="fused_ws", tile_cols=32, sweeps=24, half_keys=1,
-                        stream_threads=768, row_table=2)),
+                        stream_threads=768, row_table=2), 3),
+    # r = 5, file-major: half-key tiles with the even split
+    (11, "file", dict(kernel="fused_ws", tile_cols=128, sweeps=30, half_keys=1,
+                      stream_threads=512), 5),
+    (13, "file", dict(kernel="fused_ws", tile_cols=32, sweeps=24, half_keys=1), 5),
+    (15, "file", dict(kernel="fused_ws", tile_cols=16, sweeps=24, half_keys=1), 5),
+    (11, "worker", dict(kernel="fused"), 5),
     # beyond what any warp-specialised plan holds: the generic single pass
-    (29, "worker", dict(kernel="fused", tile_cols=8, row_table=2)),
-    (30, "worker", dict(kernel="fused", tile_cols=8, row_table=2)),
+    (29, "worker", dict(kernel="fused", tile_cols=8, row_table=2), 3),
+    (30, "worker", dict(kernel="fused", tile_cols=8, row_table=2), 3),
 ])
-def test_workload_plans(K, layout, expect):
-    sp, _ = aspis.plan(K, 3, 4096, layout)
+def test_workload_plans(K, layout, expect, r):
+    sp, _ = aspis.plan(K, r, 4096, layout)
     assert {k: sp[k] for k in expect} == expect, sp
 
 
