@@ -236,6 +236,12 @@ def main() -> int:
     ap.add_argument("--alie-z", type=float, default=None,
                     help="ALIE shift z of the colluders' value mu - z*sigma (default: the "
                          "workload's, 1.0); z = 0 puts it at the honest mean, next to the median")
+    ap.add_argument("--dist", choices=["normal", "student3", "tied"], default=None,
+                    help="honest gradient distribution (default: the workload's); tied: every "
+                         "value shares its high 16 bits, the worst case of half-key tiles")
+    ap.add_argument("--keys", choices=["auto", "half", "full"], default="auto",
+                    help="median tiles: chosen by the library's tie probe (auto), half keys "
+                         "wherever the plan has them, or full 32-bit keys")
     ap.add_argument("--mode", choices=["median", "mean", "paper"], default="median",
                     help="reduction: median (default), mean, or paper (mean when detection "
                          "succeeds, else median)")
@@ -285,6 +291,11 @@ def main() -> int:
     if args.alie_z is not None:
         import dataclasses
         wl = dataclasses.replace(wl, alie_z=args.alie_z)
+    if args.dist is not None:
+        import dataclasses
+        wl = dataclasses.replace(wl, dist={"normal": synth.DIST_NORMAL,
+                                           "student3": synth.DIST_STUDENT3,
+                                           "tied": synth.DIST_TIED}[args.dist])
     K, r, q, d, f = wl.K, wl.r, wl.q, wl.d, wl.f
     subsets = aspis.assign(K, r)
     role, worker, A, D = synth.make_roles(wl, subsets, seed=args.seed)
@@ -319,7 +330,8 @@ def main() -> int:
     out = torch.empty(d, dtype=torch.float32, device=dev)
     sel = torch.empty(f, dtype=torch.int32, device=dev)
     ws = aspis.workspace(K, r, d, dev)
-    flags = aspis.FLAG_TIMING | (aspis.FLAG_TWO_PASS if args.two_pass else 0)
+    flags = (aspis.FLAG_TIMING | (aspis.FLAG_TWO_PASS if args.two_pass else 0)
+             | {"auto": 0, "half": aspis.FLAG_HALF_KEYS, "full": aspis.FLAG_FULL_KEYS}[args.keys])
 
     def step():
         return aspis.detect_aggregate(grads, K, r, q, mode=args.mode, flags=flags, bufs=bufs,
@@ -401,11 +413,13 @@ def main() -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": ("synthetic (seeded Philox, written on the GPU): "
-                 + ("Student-t(3)" if wl.dist == synth.DIST_STUDENT3 else "Irwin-Hall N(0,0.01^2)")
+                 + {synth.DIST_STUDENT3: "Student-t(3)", synth.DIST_TIED: "tied (1 + 16 random bits)"}
+                 .get(wl.dist, "Irwin-Hall N(0,0.01^2)")
                  + f" honest gradients, {wl.distortion} adversaries"),
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
                    **({"adversary_late": min(args.adversary_late, d)}
                       if args.adversary_late > 0 else {}),
+                   **({"dist": args.dist} if args.dist else {}),
                    "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
                    **({"alie_z": wl.alie_z} if "alie" in wl.distortion else {}),
@@ -414,7 +428,8 @@ def main() -> int:
         "path": {"fused": bool(last["fused"]), "speculation_hit": bool(last["speculation_hit"]),
                  "ms_probe": round(last["ms_probe"], 4),
                  "ms_fallback": round(last["ms_fallback"], 4),
-                 "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"])},
+                 "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"]),
+                 "tie_rows": int(last["tie_rows"]), "keys": args.keys},
         "roofline": roofline,
         "fallback": fallback,
         "read_ceiling": ceiling,

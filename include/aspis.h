@@ -173,10 +173,17 @@ typedef struct {
                                   that produced out (0: the mean)          */
     int32_t half_keys;         /* 1 if that tile held only the high 16 bits
                                   of each key (low halves read back)       */
+    int32_t tie_rows;          /* tie probe: over the probed coordinates,
+                                  the median of the number of files whose
+                                  value shares the high 16-bit key half of
+                                  the files' median; -1 if not probed     */
 } aspis_run_stats;
 
 #define ASPIS_FLAG_TWO_PASS 1u   /* force detect, clique, then aggregate    */
 #define ASPIS_FLAG_TIMING 2u     /* fill the ms_* fields of stats           */
+#define ASPIS_FLAG_FULL_KEYS 4u  /* median tiles of 32-bit keys only        */
+#define ASPIS_FLAG_HALF_KEYS 8u  /* half-key tiles wherever the plan has
+                                    them, without the tie probe             */
 
 /* The whole step in one call (Algorithm 3 then Algorithm 1): agreement,
  * host clique, selection and reduction, with the same outputs as
@@ -185,6 +192,12 @@ typedef struct {
  * prefix, reduces with that guess while checking agreement on all
  * coordinates, and reruns the reduction if the full detection disagrees
  * with the guess -- the result is exact either way.
+ * Median tiles: the half-key tiles keep only the high 16 bits of each key
+ * in LDS (twice the columns) and read back the low halves of the rows tied
+ * with the median's high half.  Unless a key flag says otherwise, a tie
+ * probe over the prefix decides: when at a typical probed coordinate 64 or
+ * more files share the median's high half, the step takes full-key tiles
+ * (no read-back).  The choice changes the speed, never the result.
  *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
  *   flags   ASPIS_FLAG_* ; stats may be NULL.
  * Errors as aspis_aggregate's, except that on NO_FILES `out` holds no
@@ -255,7 +268,9 @@ aspis_status aspis_detect_aggregate_wm(const float *grads_wm, int32_t K, int32_t
                                        aspis_run_stats *stats, void *stream);
 
 /* The kernels the device entry points take for a shape, decided without
- * launching anything (host only; assumes a 16-byte aligned tensor).
+ * launching anything (host only; assumes a 16-byte aligned tensor; flags:
+ * ASPIS_FLAG_FULL_KEYS gives the full-key plans, otherwise the half-key
+ * plans the tie probe keeps for untied data).
  *   single_pass  the single-pass kernel of aspis_detect_aggregate (worker-
  *                major: aspis_detect_aggregate_wm) for the median, or
  *                ASPIS_KERNEL_NONE when the shape takes the two-pass path
@@ -282,7 +297,8 @@ typedef struct {
 } aspis_kernel_plan;
 
 aspis_status aspis_plan(int32_t K, int32_t r, int64_t d, int32_t worker_major,
-                        aspis_kernel_plan *single_pass, aspis_kernel_plan *median);
+                        uint32_t flags, aspis_kernel_plan *single_pass,
+                        aspis_kernel_plan *median);
 
 /* Diagnostic: streams nbytes (multiple of 16) of device memory and writes a
  * checksum word per thread to sink (device, >= aspis_read_probe_sink_words()

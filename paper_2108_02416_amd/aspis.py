@@ -22,6 +22,8 @@ REDUCE = {"median": 0, "mean": 1, "paper": 2}
 ATTACK = {"weak": 0, "optimal": 1}
 FLAG_TWO_PASS = 1
 FLAG_TIMING = 2
+FLAG_FULL_KEYS = 4
+FLAG_HALF_KEYS = 8
 
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
@@ -79,7 +81,7 @@ class RunStats(ctypes.Structure):
                 ("probe_coords", ctypes.c_int64), ("ms_probe", ctypes.c_float),
                 ("ms_main", ctypes.c_float), ("ms_fallback", ctypes.c_float),
                 ("ms_total", ctypes.c_float), ("tile_cols", ctypes.c_int32),
-                ("half_keys", ctypes.c_int32)]
+                ("half_keys", ctypes.c_int32), ("tie_rows", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -147,7 +149,7 @@ def lib():
     L.aspis_detect_aggregate_noalloc.restype = ctypes.c_int
     L.aspis_worker_rows.argtypes = [i32, i32, P, i64]
     L.aspis_worker_rows.restype = ctypes.c_int
-    L.aspis_plan.argtypes = [i32, i32, i64, i32, ctypes.POINTER(KernelPlan),
+    L.aspis_plan.argtypes = [i32, i32, i64, i32, u32, ctypes.POINTER(KernelPlan),
                              ctypes.POINTER(KernelPlan)]
     L.aspis_plan.restype = ctypes.c_int
     L.aspis_read_probe_sink_words.argtypes = []
@@ -196,11 +198,12 @@ def worker_rows(K: int, r: int) -> np.ndarray:
     return out
 
 
-def plan(K: int, r: int, d: int, layout: str = "file") -> tuple[dict, dict]:
+def plan(K: int, r: int, d: int, layout: str = "file", flags: int = 0) -> tuple[dict, dict]:
     """The kernels the device entry points take for this shape (aspis_plan):
-    (single pass, median), each a dict of the kernel's tile parameters."""
+    (single pass, median), each a dict of the kernel's tile parameters;
+    flags may hold FLAG_FULL_KEYS."""
     sp, med = KernelPlan(), KernelPlan()
-    _check(lib().aspis_plan(K, r, d, 1 if layout == "worker" else 0, ctypes.byref(sp),
+    _check(lib().aspis_plan(K, r, d, 1 if layout == "worker" else 0, flags, ctypes.byref(sp),
                             ctypes.byref(med)))
     return sp.as_dict(), med.as_dict()
 

@@ -160,6 +160,27 @@ bool use_mean(aspis_reduce mode, const aspis_clique_result *res) {
     return mode == ASPIS_REDUCE_MEAN || (mode == ASPIS_REDUCE_PAPER && res->success);
 }
 
+// Full-key tiles when at a typical probed coordinate at least this many
+// files share the high 16-bit key half of the median.  Below it the
+// half-key tiles' read-back stays small: 28 files tied with the median
+// (ALIE colluders sending the honest mean, K = 15) cost the half-key single
+// pass as much as the full-key one.
+constexpr uint32_t kTieFullKeys = 64;
+
+// The tie estimate: the median over the probed coordinates of the number
+// of files tied with the median's high key half (launch_tie_probe).
+uint32_t tie_estimate(const uint32_t *counts, int n) {
+    uint32_t v[aspis::kTieCols];
+    for (int j = 0; j < n; ++j) v[j] = counts[j];
+    for (int j = 1; j < n; ++j)
+        for (int i = j; i > 0 && v[i - 1] > v[i]; --i) {
+            const uint32_t t = v[i];
+            v[i] = v[i - 1];
+            v[i - 1] = t;
+        }
+    return n > 0 ? v[n / 2] : 0u;
+}
+
 aspis_status check_detect_out(const aspis_detect_out *o) {
     if (!o || !o->pair_diff || !o->vote || !o->has_majority || !o->disagree)
         return fail(ASPIS_ERR_INVALID_ARG, "detect outputs must all be non-NULL");
@@ -304,7 +325,8 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
                             int64_t d, const int32_t *subsets_dev, const aspis_detect_out *det,
                             const aspis_clique_result *res, aspis_reduce mode, float *out,
                             int32_t *sel_out, int64_t *n_selected, void *workspace,
-                            size_t ws_bytes, void *stream, aspis::TileUse *use = nullptr) {
+                            size_t ws_bytes, void *stream, aspis::TileUse *use = nullptr,
+                            bool full_keys = false) {
     int64_t f = 0;
     aspis_status st = check_device_shape(K, r, d, &f);
     if (st != ASPIS_OK) return st;
@@ -329,7 +351,7 @@ aspis_status aggregate_impl(const float *grads, const int32_t *row_of, int32_t K
     if (mean)
         ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
     else
-        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, use));
+        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, use, full_keys));
     return ASPIS_OK;
 }
 
@@ -368,14 +390,35 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     hipEvent_t *ev = events.e;
     if (timing)
         for (int i = 0; i < 6; ++i) ASPIS_HIP(hipEventCreate(&ev[i]));
-    uint64_t rows[ASPIS_MAX_K_DEVICE];
+    aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
+    // key tiles: full keys when asked, half keys when asked, else chosen
+    // from the tie probe run with the first agreement pass
+    bool full_keys = (flags & ASPIS_FLAG_FULL_KEYS) != 0;
+    const bool tie_probe =
+        (flags & (ASPIS_FLAG_FULL_KEYS | ASPIS_FLAG_HALF_KEYS)) == 0 && mode != ASPIS_REDUCE_MEAN;
+    const int64_t probe = probe_coords(f, d);
+    const int n_tie = (int)(probe < aspis::kTieCols ? probe : aspis::kTieCols);
+    uint32_t *tie_dev = reinterpret_cast<uint32_t *>(ws.stage + aspis::kStageTie);
+    local.tie_rows = -1;
+    auto decide_keys = [&](const uint64_t *staged_words) {
+        if (!tie_probe) return;
+        const uint32_t t = tie_estimate(
+            reinterpret_cast<const uint32_t *>(staged_words + aspis::kStageTie), n_tie);
+        local.tie_rows = (int32_t)t;
+        full_keys = t >= kTieFullKeys;
+    };
+    // the two-pass path: the disagreement rows and the tie counts, one sync
+    uint64_t rows[aspis::kStageWords] = {};
     auto graph_to_host = [&](aspis_clique_result *out_res) -> aspis_status {
         ASPIS_HIP(hipMemcpyAsync(rows, det->disagree, sizeof(uint64_t) * K,
                                  hipMemcpyDeviceToHost, s));
+        if (tie_probe)
+            ASPIS_HIP(hipMemcpyAsync(rows + aspis::kStageTie, tie_dev, sizeof(uint32_t) * n_tie,
+                                     hipMemcpyDeviceToHost, s));
         ASPIS_HIP(hipStreamSynchronize(s));
+        decide_keys(rows);
         return aspis_clique(rows, K, q, out_res);
     };
-    aspis::Workspace ws = aspis::carve_workspace(workspace, f, r);
     // the row of every replica in a worker-major upload, in the workspace.
     // The host copy must outlive the asynchronous upload: the guard, declared
     // after it and so destroyed before it, waits for the stream on every
@@ -403,22 +446,27 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     if (try_fused) {
         // the detection rows of the last vote, staged in the workspace by
         // vote_rows_kernel, with stage[64] = "some vote changed"
-        uint64_t staged[65] = {};
-        auto staged_clique = [&](aspis_clique_result *out_res) -> aspis_status {
-            ASPIS_HIP(hipMemcpyAsync(staged, ws.stage, sizeof staged, hipMemcpyDeviceToHost, s));
+        uint64_t staged[aspis::kStageWords] = {};
+        auto staged_clique = [&](aspis_clique_result *out_res, int words) -> aspis_status {
+            ASPIS_HIP(hipMemcpyAsync(staged, ws.stage, sizeof(uint64_t) * words,
+                                     hipMemcpyDeviceToHost, s));
             ASPIS_HIP(hipStreamSynchronize(s));
             return aspis_clique(staged, K, q, out_res);
         };
-        // 1) agreement on a coordinate prefix -> provisional clique and selection
-        const int64_t probe = probe_coords(f, d);
+        // 1) agreement on a coordinate prefix -> provisional clique and
+        //    selection; the tie probe rides on the same copy to the host
         local.probe_coords = probe;
         if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
         ASPIS_HIP(aspis::launch_agree_file(grads, row_of, f, r, d, probe, det->pair_diff, s));
         ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
                                           det->has_majority, det->disagree, ws.stage, s));
+        if (tie_probe)
+            ASPIS_HIP(aspis::launch_tie_probe(grads, row_of, f, r, d, probe, tie_dev, s));
         if (timing) ASPIS_HIP(hipEventRecord(ev[1], s));
         aspis_clique_result guess{};
-        if ((st = staged_clique(&guess)) != ASPIS_OK) return st;
+        if ((st = staged_clique(&guess, tie_probe ? aspis::kStageWords : 65)) != ASPIS_OK)
+            return st;
+        decide_keys(staged);
         // the reduction the guess calls for: the median (Case 2, or MEDIAN
         // mode) or the mean (Case 1 in PAPER mode, or MEAN mode)
         const bool guess_mean = use_mean(mode, &guess);
@@ -437,11 +485,11 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 ASPIS_HIP(aspis::launch_fused_mean(grads, row_of, f, r, d, ws, det->pair_diff, out, s));
             else
                 ASPIS_HIP(aspis::launch_fused(grads, row_of, f, r, d, ws, det->pair_diff, out, s,
-                                              &fused_tile));
+                                              &fused_tile, full_keys));
             if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
             ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
                                               det->has_majority, det->disagree, ws.stage, s));
-            if ((st = staged_clique(res)) != ASPIS_OK) return st;
+            if ((st = staged_clique(res, 65)) != ASPIS_OK) return st;
             const bool vote_changed = staged[64] != 0;
             // 3) the final selection.  The guess selected the same replica of
             //    every file iff both detections took the same case and
@@ -468,7 +516,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 if (use_mean(mode, res))
                     ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
                 else
-                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile));
+                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile, full_keys));
             }
             local.tile_cols = fused_tile.cols;
             local.half_keys = fused_tile.half;
@@ -487,10 +535,12 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     // two-pass: full agreement, clique, then selection and reduction
     if (timing) ASPIS_HIP(hipEventRecord(ev[2], s));
     if ((st = detect_impl(grads, row_of, K, r, d, subsets_dev, det, stream)) != ASPIS_OK) return st;
+    if (tie_probe)
+        ASPIS_HIP(aspis::launch_tie_probe(grads, row_of, f, r, d, probe, tie_dev, s));
     if ((st = graph_to_host(res)) != ASPIS_OK) return st;
     aspis::TileUse tile{};
     st = aggregate_impl(grads, row_of, K, r, d, subsets_dev, det, res, mode, out, sel_out,
-                        n_selected, workspace, ws_bytes, stream, &tile);
+                        n_selected, workspace, ws_bytes, stream, &tile, full_keys);
     local.tile_cols = tile.cols;
     local.half_keys = tile.half;
     if (timing) ASPIS_HIP(hipEventRecord(ev[3], s));
@@ -599,16 +649,18 @@ static void to_abi(const aspis::KernelPlan &k, aspis_kernel_plan *out) {
     out->lds_bytes = k.lds_bytes;
 }
 
-aspis_status aspis_plan(int32_t K, int32_t r, int64_t d, int32_t worker_major,
+aspis_status aspis_plan(int32_t K, int32_t r, int64_t d, int32_t worker_major, uint32_t flags,
                         aspis_kernel_plan *single_pass, aspis_kernel_plan *median) {
     int64_t f = 0;
     aspis_status st = check_device_shape(K, r, d, &f);
     if (st != ASPIS_OK) return st;
     if (!single_pass || !median) return fail(ASPIS_ERR_INVALID_ARG, "aspis_plan: NULL output");
     const bool vec = d % 4 == 0;
+    const bool full_keys = (flags & ASPIS_FLAG_FULL_KEYS) != 0;
     aspis::KernelPlan fused{}, med{};
-    if (f <= aspis::kVoteRowsMaxFiles) aspis::plan_fused(f, r, vec, worker_major != 0, &fused);
-    aspis::plan_median(f, vec, &med);
+    if (f <= aspis::kVoteRowsMaxFiles)
+        aspis::plan_fused(f, r, vec, worker_major != 0, &fused, full_keys);
+    aspis::plan_median(f, vec, &med, full_keys);
     to_abi(fused, single_pass);
     to_abi(med, median);
     if (fused.kind == aspis::kKernelUnbuilt || med.kind == aspis::kKernelUnbuilt)

@@ -25,9 +25,13 @@ struct Workspace {
     int32_t *pos;     // [f] row of the file in the kept-file list, or -1
     int32_t *rows;    // [f] kept replica rows (i*r + slot), file order
     int32_t *n_sel;   // [1] number of kept files
-    uint64_t *stage;  // [65] disagreement rows and a flag, staged for the host
+    uint64_t *stage;  // [104] staged for the host: [0,64) disagreement rows,
+                      // [64] a vote-changed flag, [72,104) the tie probe's
+                      // kTieCols uint32 counts (kStageTie)
     int32_t *row_of;  // [f*r] row of replica (i,s) in a worker-major upload
 };
+constexpr int kStageTie = 72;      // first stage word of the tie counts
+constexpr int kStageWords = 104;   // stage words the host reads back
 size_t workspace_bytes(int64_t f, int r);
 Workspace carve_workspace(void *base, int64_t f, int r);
 
@@ -98,13 +102,15 @@ struct KernelPlan {
 };
 // Median over up to f kept rows (always has a kernel); single pass for f
 // files of r replicas (false: none, the step then takes two passes).  vec:
-// d % 4 == 0 and a 16-byte aligned tensor; ind: rows through a row table.
-bool plan_median(int64_t f, bool vec, KernelPlan *out);
-bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out);
+// d % 4 == 0 and a 16-byte aligned tensor; ind: rows through a row table;
+// full_keys: tiles of 32-bit keys only (no half-key plan, no read-back).
+bool plan_median(int64_t f, bool vec, KernelPlan *out, bool full_keys = false);
+bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out, bool full_keys = false);
 
 // Coordinate-wise lower median / fp64 mean of the kept rows.
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,
-                         int64_t f, float *out, hipStream_t s, TileUse *use = nullptr);
+                         int64_t f, float *out, hipStream_t s, TileUse *use = nullptr,
+                         bool full_keys = false);
 hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
                        float *out, hipStream_t s);
 
@@ -112,7 +118,7 @@ hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
 // the rows selected by ws (a guess), in one read of the replica tensor.
 hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         const Workspace &ws, uint32_t *pair_diff, float *out,
-                        hipStream_t s, TileUse *use = nullptr);
+                        hipStream_t s, TileUse *use = nullptr, bool full_keys = false);
 bool fused_supported(int64_t f, int r);
 
 // Single pass with the mean: agreement bits of every file over [0, d) and
@@ -128,6 +134,14 @@ bool fused_mean_supported(int64_t f, int r);
 // up on the first call per device (the calling thread's current device).
 constexpr size_t kScratchBytes = (size_t)2 << 20;
 hipError_t scratch_ptr(void **out);
+
+// Tie probe over coordinates [0, kend): for min(kTieCols, kend) coordinates
+// spread over them, out[j] = the number of files whose value (the value of
+// its largest class of equal replicas) shares the high 16-bit key half of
+// those values' lower median.  The host reads out[0 .. min(kTieCols, kend)).
+constexpr int kTieCols = 64;
+hipError_t launch_tie_probe(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                            int64_t kend, uint32_t *out, hipStream_t s);
 
 size_t read_probe_sink_words();
 hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink,

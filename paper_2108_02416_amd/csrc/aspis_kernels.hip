@@ -1683,6 +1683,96 @@ median_radix_kernel(const float *__restrict__ g, int64_t d, const int32_t *__res
 }
 
 // ---------------------------------------------------------------------------
+// tie probe: how many values share the median's high 16 key bits.  The
+// half-key tiles read back the low halves of every row tied with the
+// median's high half, so heavily tied data (quantised gradients, values on
+// a grid) is better served by full-key tiles.  For kTieCols coordinates
+// spread over the probed prefix, one workgroup takes each file's value at
+// that coordinate -- the value of its largest class of equal replicas, the
+// file's vote on that coordinate alone, which is what the selection keeps
+// in most files -- finds the high half H of their lower median (two
+// 8-bit histogram rounds in LDS) and stores how many files have high half
+// H.  It needs no selection, so it runs with the probe.
+
+constexpr int kTieThreads = 256;
+constexpr int kTieMaxFiles = 4096;   // files looked at per coordinate (the first ones)
+static_assert(kTieThreads == 256, "one histogram bucket per thread");
+
+template <int R>
+__global__ void __launch_bounds__(kTieThreads)
+tie_probe_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
+                 int64_t d, int64_t kstep, uint32_t *__restrict__ out) {
+    __shared__ uint16_t h[kTieMaxFiles];
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t wsum[kTieThreads / 64];
+    __shared__ uint32_t pick[2];   // bucket, rank within it
+    const int tid = threadIdx.x;
+    const int64_t k = (int64_t)blockIdx.x * kstep;   // < d (host)
+    const int n = (int)(f < kTieMaxFiles ? f : kTieMaxFiles);
+    for (int i = tid; i < n; i += kTieThreads) {
+        uint32_t v[R];
+#pragma unroll
+        for (int s = 0; s < R; ++s) v[s] = __float_as_uint(g[replica_row(row_of, i, R, s) * d + k]);
+        // the value of the largest class of equal replicas, the lower slot
+        // on a tie (Eq. (3) on this one coordinate)
+        uint32_t val = v[0];
+        int best = 0;
+#pragma unroll
+        for (int s = 0; s < R; ++s) {
+            int c = 0;
+#pragma unroll
+            for (int t = 0; t < R; ++t) c += v[s] == v[t] ? 1 : 0;
+            if (c > best) {
+                best = c;
+                val = v[s];
+            }
+        }
+        h[i] = (uint16_t)(to_key(val) >> 16);
+    }
+    // round 0 counts the high bytes; round 1 the low bytes of the keys whose
+    // high byte is the median's; the median's bucket count then is the number
+    // of files tied with it
+    uint32_t rank = (uint32_t)(n - 1) / 2, hi = 0u;
+    for (int round = 0; round < 2; ++round) {
+        hist[tid] = 0u;   // kTieThreads == 256 buckets
+        __syncthreads();
+        for (int i = tid; i < n; i += kTieThreads) {
+            const uint32_t x = h[i];
+            if (round == 0)
+                atomicAdd(&hist[x >> 8], 1u);
+            else if ((x >> 8) == hi)
+                atomicAdd(&hist[x & 255u], 1u);
+        }
+        __syncthreads();
+        // the bucket holding the rank: a prefix sum over the 256 buckets,
+        // one per thread (wave scans, then the waves' totals)
+        const uint32_t c = hist[tid];
+        uint32_t incl = c;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)incl, o, 64);
+            incl += (tid & 63) >= o ? y : 0u;
+        }
+        if ((tid & 63) == 63) wsum[tid >> 6] = incl;
+        __syncthreads();
+        for (int w = 0; w < (tid >> 6); ++w) incl += wsum[w];
+        if (incl - c <= rank && rank < incl) {   // exactly one bucket
+            pick[0] = (uint32_t)tid;
+            pick[1] = rank - (incl - c);
+        }
+        __syncthreads();
+        const uint32_t b = pick[0];
+        if (round == 0) {
+            hi = b;
+            rank = pick[1];
+        } else if (tid == 0) {
+            out[blockIdx.x] = hist[b];
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
 // read-bandwidth probe
 
 constexpr int kProbeBlocks = 2048;
@@ -1937,7 +2027,7 @@ int64_t mws_lds_bytes(int64_t f, int T, bool half, int fill) {
                 : (hist_words(T) + f * (int64_t)T) * 4 + f * 4;
 }
 
-WsPlan mws_plan(int64_t f, bool vec) {
+WsPlan mws_plan(int64_t f, bool vec, bool full_keys = false) {
     WsPlan p;
     if (!vec) return p;
     for (int T : {64, 32, 16, 8}) {
@@ -1950,6 +2040,7 @@ WsPlan mws_plan(int64_t f, bool vec) {
         p.sweeps = sw <= 4 ? 4 : sw <= 8 ? 8 : sw <= 12 ? 12 : 16;
         break;
     }
+    if (full_keys) return p;
     const WsPlan h = half_plan(f, p.T, false, false, [&](int T, int fill) {
         return mws_lds_bytes(f, T, true, fill);
     });
@@ -1971,10 +2062,10 @@ int64_t ws_lds_bytes(int64_t f, int r, int T, bool table_in_lds, bool half, int 
 // median above (the wide split without a row table in LDS).  r = 5: half-key
 // tiles of the file-major tensor, even split (five 16-byte chunks a sweep
 // leave the streaming role no registers for more).
-WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
+WsPlan ws_plan(int64_t f, int r, bool vec, bool ind, bool full_keys = false) {
     WsPlan p;
     if (!vec) return p;
-    if (r == 5 && !ind) {
+    if (r == 5 && !ind && !full_keys) {
         p.r = 5;
         WsPlan h = half_plan(f, 0, false, false, [&](int T, int fill) {
             return ws_lds_bytes(f, r, T, false, true, fill);
@@ -1992,6 +2083,7 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind) {
         p.sweeps = round_sweeps(sw, false, T, kWsFill);
         break;
     }
+    if (full_keys) return p;
     const WsPlan h = half_plan(f, p.T, ind, false, [&](int T, int fill) {
         return ws_lds_bytes(f, r, T, ind, true, fill);
     });
@@ -2177,8 +2269,8 @@ KernelPlan ws_kernel_plan(int kind, const WsPlan &p, int64_t lds, int table) {
 
 }  // namespace
 
-bool plan_median(int64_t f, bool vec, KernelPlan *out) {
-    const WsPlan p = mws_plan(f, vec);
+bool plan_median(int64_t f, bool vec, KernelPlan *out, bool full_keys) {
+    const WsPlan p = mws_plan(f, vec, full_keys);
     if (p.T != 0) {
         *out = ws_kernel_plan(median_ws_fn(p) ? kKernelMedianWs : kKernelUnbuilt, p,
                               mws_lds_bytes(f, p.T, p.half, p.fill), 0);
@@ -2201,9 +2293,9 @@ bool plan_median(int64_t f, bool vec, KernelPlan *out) {
     return true;
 }
 
-bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out) {
+bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out, bool full_keys) {
     *out = KernelPlan{};
-    const WsPlan p = ws_plan(f, r, vec, ind);
+    const WsPlan p = ws_plan(f, r, vec, ind, full_keys);
     if (p.T != 0) {
         const int table = ind ? (p.rtg ? 2 : 1) : 0;
         *out = ws_kernel_plan(fused_ws_fn(p, ind) ? kKernelFusedWs : kKernelUnbuilt, p,
@@ -2227,16 +2319,16 @@ bool fused_supported(int64_t f, int r) {
 }
 
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
-                         float *out, hipStream_t s, TileUse *use) {
+                         float *out, hipStream_t s, TileUse *use, bool full_keys) {
     const bool vec = (d % 4 == 0) && aligned16(g);
     KernelPlan k;
-    if (!plan_median(f, vec, &k)) return hipErrorInvalidValue;
+    if (!plan_median(f, vec, &k, full_keys)) return hipErrorInvalidValue;
     if (use) *use = TileUse{k.tile_cols, k.half_keys};
     const int T = k.tile_cols;
     const int64_t ntiles = (d + T - 1) / T;
     if (k.kind == kKernelMedianWs) {
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-        const MedianWsFn fn = median_ws_fn(mws_plan(f, vec));
+        const MedianWsFn fn = median_ws_fn(mws_plan(f, vec, full_keys));
         fn<<<grid, kWsThreads, (size_t)k.lds_bytes, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
         return hipGetLastError();
     }
@@ -2269,18 +2361,18 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
 
 hipError_t launch_fused(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         const Workspace &ws, uint32_t *pair_diff, float *out, hipStream_t s,
-                        TileUse *use) {
+                        TileUse *use, bool full_keys) {
     const bool vec = (d % 4 == 0) && aligned16(g);
     const bool ind = row_of != nullptr;
     KernelPlan k;
-    if (!plan_fused(f, r, vec, ind, &k)) return hipErrorInvalidValue;
+    if (!plan_fused(f, r, vec, ind, &k, full_keys)) return hipErrorInvalidValue;
     if (use) *use = TileUse{k.tile_cols, k.half_keys};
     const int T = k.tile_cols;
     const int64_t ntiles = (d + T - 1) / T;
     const size_t lds = (size_t)k.lds_bytes;
     if (k.kind == kKernelFusedWs) {
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
-        const FusedWsFn fn = fused_ws_fn(ws_plan(f, r, vec, ind), ind);
+        const FusedWsFn fn = fused_ws_fn(ws_plan(f, r, vec, ind, full_keys), ind);
         fn<<<grid, kWsThreads, lds, s>>>(g, ind ? row_of : nullptr, f, d, ws.sel, ws.pos, ws.n_sel,
                                          ntiles, pair_diff, out);
         return hipGetLastError();
@@ -2380,6 +2472,20 @@ hipError_t scratch_ptr(void **out) {
     }
     *out = p;
     return hipSuccess;
+}
+
+hipError_t launch_tie_probe(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                            int64_t kend, uint32_t *out, hipStream_t s) {
+    if (f <= 0 || kend <= 0) return hipErrorInvalidValue;
+    const int64_t kstep = kend >= kTieCols ? kend / kTieCols : 1;
+    const unsigned grid = (unsigned)(kend >= kTieCols ? kTieCols : kend);
+    switch (r) {
+    case 3: tie_probe_kernel<3><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
+    case 5: tie_probe_kernel<5><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
+    case 7: tie_probe_kernel<7><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 size_t read_probe_sink_words() { return (size_t)kProbeBlocks * kBlock; }

@@ -35,7 +35,7 @@ _LIB_PATH = os.path.join(HERE, "libsynth.so")
 _lib = None
 
 ROLE_HONEST, ROLE_REVERSED, ROLE_ALIE, ROLE_NOISE = 0, 1, 2, 3
-DIST_NORMAL, DIST_STUDENT3 = 0, 1
+DIST_NORMAL, DIST_STUDENT3, DIST_TIED = 0, 1, 2
 SEED = 428          # the paper's primary seed (its repeat seed is 50)
 SEED_REPEAT = 50
 

@@ -13,7 +13,10 @@ extern "C" {
 
 enum { SYNTH_ROLE_HONEST = 0, SYNTH_ROLE_REVERSED = 1, SYNTH_ROLE_ALIE = 2,
        SYNTH_ROLE_NOISE = 3 };
-enum { SYNTH_DIST_NORMAL = 0, SYNTH_DIST_STUDENT3 = 1 };
+/* NORMAL: 0.01 * N(0,1); STUDENT3: 0.01 * t(3); TIED: 1 + u * 2^-23 with a
+ * 16-bit uniform u, i.e. every value shares the high 16 bits 0x3F80 of its
+ * binary32 pattern (the heaviest ties a half-key tile can meet). */
+enum { SYNTH_DIST_NORMAL = 0, SYNTH_DIST_STUDENT3 = 1, SYNTH_DIST_TIED = 2 };
 
 /* One 32-bit draw, for seeded choices (adversary sets, permutations). */
 uint32_t synth_u32(uint64_t seed, uint32_t stream, uint64_t index);

@@ -21,6 +21,9 @@
  *   honest   g_i[k] = fl32(0.01 * Z)                         (dist 0)
  *                     fl32(0.01 * Z0 / sqrt((Z1^2+Z2^2+Z3^2)/3)), a
  *                     Student-t with 3 degrees of freedom     (dist 1)
+ *                     the binary32 pattern 0x3F800000 | (16 random bits),
+ *                     values in [1, 1 + 2^-7) sharing their high 16 bits
+ *                                                             (dist 2)
  *   reversed -100 * g_i[k] (binary32 multiply)
  *   ALIE     fl32(mu_k - z * sigma_k): mean and population std of the f
  *            honest g_i[k], fp64, files in ascending order (same vector for
@@ -80,6 +83,14 @@ __host__ __device__ inline double normal(uint64_t seed, uint32_t stream, uint32_
 
 __host__ __device__ inline float honest_value(uint64_t seed, int32_t dist, uint32_t file,
                                               uint64_t k) {
+    if (dist == SYNTH_DIST_TIED) {
+        // 1 + (16 random bits) * 2^-23: the bit pattern 0x3F80xxxx
+        const U4 u = philox(seed, (uint32_t)k, (uint32_t)(k >> 32), file, 1u << 8);
+        const uint32_t bits = 0x3F800000u | (u.x[0] & 0xFFFFu);
+        float v;
+        __builtin_memcpy(&v, &bits, sizeof v);
+        return v;
+    }
     if (dist == SYNTH_DIST_STUDENT3) {
         const double z0 = normal(seed, 1u, 0u, file, k);
         const double z1 = normal(seed, 1u, 1u, file, k);

@@ -32,24 +32,24 @@ hipError_t launch_select(const int32_t *, const int8_t *, int64_t, int, int, uin
                          hipStream_t) {
     return hipErrorInvalidValue;
 }
-bool plan_median(int64_t, bool, KernelPlan *out) {
+bool plan_median(int64_t, bool, KernelPlan *out, bool) {
     *out = KernelPlan{};
     out->kind = kKernelMedianRadix;
     return true;
 }
-bool plan_fused(int64_t, int, bool, bool, KernelPlan *out) {
+bool plan_fused(int64_t, int, bool, bool, KernelPlan *out, bool) {
     *out = KernelPlan{};
     return false;
 }
 hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, float *, hipStream_t,
-                         TileUse *) {
+                         TileUse *, bool) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_mean(const float *, int64_t, const Workspace &, float *, hipStream_t) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_fused(const float *, const int32_t *, int64_t, int, int64_t, const Workspace &,
-                        uint32_t *, float *, hipStream_t, TileUse *) {
+                        uint32_t *, float *, hipStream_t, TileUse *, bool) {
     return hipErrorInvalidValue;
 }
 bool fused_supported(int64_t, int) { return false; }
@@ -59,6 +59,10 @@ hipError_t launch_fused_mean(const float *, const int32_t *, int64_t, int, int64
 }
 bool fused_mean_supported(int64_t, int) { return false; }
 hipError_t scratch_ptr(void **) { return hipErrorInvalidValue; }
+hipError_t launch_tie_probe(const float *, const int32_t *, int64_t, int, int64_t, int64_t,
+                            uint32_t *, hipStream_t) {
+    return hipErrorInvalidValue;
+}
 size_t read_probe_sink_words() { return 0; }
 hipError_t launch_read_probe(const void *, size_t, uint32_t *, hipStream_t) {
     return hipErrorInvalidValue;

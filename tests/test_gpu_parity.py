@@ -476,3 +476,40 @@ def test_read_probe_reads_every_chunk_once(nbytes):
     torch.cuda.synchronize()
     got = np.bitwise_xor.reduce(to_np(sink).view(np.uint32))
     assert got == np.bitwise_xor.reduce(words)
+
+
+def test_caller_buffers_are_checked():
+    """Caller-supplied outputs and buffers of the wrong size, dtype, device
+    or layout are refused by the binding before the library writes into
+    them (the kernels write d floats of out, f words of the detection
+    buffers and of sel_out)."""
+    import torch
+    wl = synth.WORKLOADS[1]
+    s = oracle.assign(wl.K, wl.r)
+    d = 260
+    g, _ = synth.generate(wl, s, d=d)
+    dev = device()
+    gd = torch.from_numpy(g).to(dev)
+    f = s.shape[0]
+    bad = [
+        dict(out=torch.empty(d - 1, dtype=torch.float32, device=dev)),
+        dict(out=torch.empty(d, dtype=torch.float64, device=dev)),
+        dict(out=torch.empty(d, dtype=torch.float32)),
+        dict(out=torch.empty(2 * d, dtype=torch.float32, device=dev)[::2]),
+        dict(sel_out=torch.empty(f - 1, dtype=torch.int32, device=dev)),
+        dict(bufs=aspis.DetectBuffers.empty(f - 1, wl.K, dev)),
+        dict(bufs=aspis.DetectBuffers.empty(f, wl.K - 1, dev)),
+        dict(ws=torch.empty(64, dtype=torch.int32, device=dev)),
+    ]
+    for kw in bad:
+        with pytest.raises(aspis.AspisError) as e:
+            aspis.detect_aggregate(gd, wl.K, wl.r, wl.q, **kw)
+        assert e.value.status == aspis.ERR_INVALID_ARG, kw
+    small_ws = torch.empty(64, dtype=torch.uint8, device=dev)
+    with pytest.raises(aspis.AspisError) as e:
+        aspis.detect_aggregate(gd, wl.K, wl.r, wl.q, ws=small_ws)
+    assert e.value.status == aspis.ERR_BUFFER_SMALL
+    # the buffers of the right shape still work after the refusals
+    got = aspis.detect_aggregate(gd, wl.K, wl.r, wl.q)
+    torch.cuda.synchronize()
+    assert_same_floats(to_np(got["out"]), oracle.run(g, wl.K, wl.r, wl.q)["out"])

@@ -255,3 +255,49 @@ def test_r5_half_key_single_pass(K, q, attack):
         assert got["stats"]["fused"] == 1
         if mode == "median":
             assert got["stats"]["tile_cols"] == T and got["stats"]["half_keys"] == 1
+
+
+@pytest.mark.parametrize("idx", [3, 4, 5])
+def test_tied_data_takes_full_keys(idx):
+    """Every honest value shares its high 16 bits (1 + 16 random bits of
+    mantissa): the tie probe sees hundreds of files tied in a typical
+    column and the step takes full-key tiles; forcing half keys instead
+    reads every low half back.  Both agree with the oracle, in the steady
+    state (every workgroup on three or more tiles), both paths."""
+    import dataclasses
+    wl = dataclasses.replace(synth.WORKLOADS[idx], dist=synth.DIST_TIED)
+    K, r, q = wl.K, wl.r, wl.q
+    sp, _ = aspis.plan(K, r, 4096, "file", aspis.FLAG_FULL_KEYS)
+    d = _steady_d(sp["tile_cols"], CUS, 4)
+    s = oracle.assign(K, r)
+    g, _ = synth.generate(wl, s, d=d)
+    assert ((g.view(np.uint32) >> 16) != 0x3F80).sum() < g.size // 2   # mostly tied
+    print(f"tied workload {idx}: f={wl.f} d={d}", flush=True)
+    ref = _oracle(g, K, r, q, "median")
+    auto = _run(g, K, r, q, "median")
+    _compare(auto, ref, K, "median")
+    assert auto["stats"]["half_keys"] == 0 and auto["stats"]["tie_rows"] >= 64, auto["stats"]
+    for flags in (aspis.FLAG_HALF_KEYS, aspis.FLAG_FULL_KEYS | aspis.FLAG_TWO_PASS,
+                  aspis.FLAG_HALF_KEYS | aspis.FLAG_TWO_PASS):
+        got = _run(g, K, r, q, "median", flags)
+        _compare(got, ref, K, "median")
+        assert got["stats"]["half_keys"] == (1 if flags & aspis.FLAG_HALF_KEYS else 0), flags
+        assert got["stats"]["tie_rows"] == -1
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5, 6])
+def test_untied_workloads_keep_half_keys(idx):
+    """The generator's workloads (continuous values, adversaries agreeing
+    on one value in at most a few dozen files) stay on the half-key plans,
+    and the tie probe runs on the two-pass path too."""
+    wl = synth.WORKLOADS[idx]
+    K, r, q = wl.K, wl.r, wl.q
+    s = oracle.assign(K, r)
+    g, _ = synth.generate(wl, s, d=4096 + 64)
+    for flags in (0, aspis.FLAG_TWO_PASS):
+        got = _run(g, K, r, q, "median", flags)
+        _compare(got, _oracle(g, K, r, q, "median"), K, "median")
+        assert 0 <= got["stats"]["tie_rows"] < 64, got["stats"]
+        sp, med = aspis.plan(K, r, 4096 + 64)
+        want = (sp if not flags else med)["half_keys"]
+        assert got["stats"]["half_keys"] == want, (got["stats"], sp, med)

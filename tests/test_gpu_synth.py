@@ -11,10 +11,15 @@ from _helpers import device
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
-def test_device_fill_matches_host_fill(idx):
+@pytest.mark.parametrize("idx,dist", [(1, None), (2, None), (3, None), (4, None), (5, None),
+                                      (6, None), (3, synth.DIST_TIED), (5, synth.DIST_TIED)])
+def test_device_fill_matches_host_fill(idx, dist):
+    import dataclasses
+
     import torch
     wl = synth.WORKLOADS[idx]
+    if dist is not None:
+        wl = dataclasses.replace(wl, dist=dist)
     s = oracle.assign(wl.K, wl.r)
     role, worker, _, _ = synth.make_roles(wl, s)
     d = 3001

@@ -24,10 +24,11 @@ def test_every_plan_maps_to_a_built_kernel():
     bad = []
     for K, r in _shapes():
         f = comb(K, r)
-        for layout in ("file", "worker"):
+        for layout, flags in (("file", 0), ("worker", 0), ("file", aspis.FLAG_FULL_KEYS),
+                              ("worker", aspis.FLAG_FULL_KEYS)):
             for d in (4096, 4097):
                 try:
-                    sp, med = aspis.plan(K, r, d, layout)
+                    sp, med = aspis.plan(K, r, d, layout, flags)
                 except aspis.AspisError as e:
                     bad.append((K, r, layout, d, str(e)))
                     continue
@@ -39,6 +40,8 @@ def test_every_plan_maps_to_a_built_kernel():
                     bad.append((K, r, layout, d, "single pass past the vote kernel", sp))
                 if d % 4 and sp["kernel"] == "fused_ws":
                     bad.append((K, r, layout, d, "warp-specialised pass on unaligned rows", sp))
+                if flags and (sp["half_keys"] or med["half_keys"]):
+                    bad.append((K, r, layout, d, "half keys despite FLAG_FULL_KEYS", sp, med))
                 if sp["kernel"] != "none" and sp["lds_bytes"] > 160 * 1024:
                     bad.append((K, r, layout, d, "LDS", sp))
                 if med["lds_bytes"] > 160 * 1024:
@@ -90,3 +93,13 @@ def test_median_plans(K, r, kernel):
     """Medians of more kept files than an LDS tile holds re-read HBM."""
     _, med = aspis.plan(K, r, 4096)
     assert med["kernel"] == kernel, med
+
+
+@pytest.mark.parametrize("K,kernel,T", [(15, "fused_ws", 64), (21, "fused_ws", 16),
+                                        (25, "fused_ws", 8)])
+def test_full_key_plans_of_the_workloads(K, kernel, T):
+    """The full-key plans the tie probe switches to on heavily tied data:
+    narrower tiles of 32-bit keys, no read-back."""
+    sp, med = aspis.plan(K, 3, 4096, "file", aspis.FLAG_FULL_KEYS)
+    assert (sp["kernel"], sp["tile_cols"], sp["half_keys"]) == (kernel, T, 0), sp
+    assert med["half_keys"] == 0, med
