@@ -301,3 +301,42 @@ def test_untied_workloads_keep_half_keys(idx):
         sp, med = aspis.plan(K, r, 4096 + 64)
         want = (sp if not flags else med)["half_keys"]
         assert got["stats"]["half_keys"] == want, (got["stats"], sp, med)
+
+
+def _tie_estimate_numpy(g: np.ndarray, probe: int) -> int:
+    """The tie probe's estimate written out with numpy: at 64 coordinates
+    spread over the probed prefix, every file's value by its vote on that
+    coordinate (largest class of bitwise-equal replicas, lower slot on a
+    tie), the high 16 bits of the totalOrder key of their lower median, and
+    the number of files sharing them; the median of the 64 counts."""
+    f, r, _ = g.shape
+    n = min(f, 4096)
+    cols = min(64, probe)
+    step = probe // 64 if probe >= 64 else 1
+    bits = g.view(np.uint32)
+    counts = []
+    for j in range(cols):
+        v = bits[:n, :, j * step]
+        eq = (v[:, :, None] == v[:, None, :]).sum(axis=2)        # class sizes per slot
+        pick = v[np.arange(n), eq.argmax(axis=1)]                # first slot of a largest class
+        key = np.where(pick >> 31, ~pick, pick | np.uint32(0x80000000)).astype(np.uint32)
+        hi = np.sort(key >> 16)
+        med = hi[(n - 1) // 2]
+        counts.append(int((hi == med).sum()))
+    return sorted(counts)[len(counts) // 2]
+
+
+@pytest.mark.parametrize("idx,dist", [(3, None), (4, None), (6, None), (3, synth.DIST_TIED),
+                                      (5, synth.DIST_TIED)])
+def test_tie_probe_estimate(idx, dist):
+    """The tie probe's count (stats tie_rows) equals the same quantity
+    computed with numpy on the generated replicas."""
+    import dataclasses
+    wl = synth.WORKLOADS[idx]
+    if dist is not None:
+        wl = dataclasses.replace(wl, dist=dist)
+    s = oracle.assign(wl.K, wl.r)
+    g, _ = synth.generate(wl, s, d=20000)
+    got = _run(g, wl.K, wl.r, wl.q, "median")
+    probe = got["stats"]["probe_coords"]
+    assert got["stats"]["tie_rows"] == _tie_estimate_numpy(g, probe), got["stats"]
