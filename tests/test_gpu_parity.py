@@ -16,7 +16,7 @@ from _helpers import assert_detection, assert_same_floats, device, to_np
 pytestmark = pytest.mark.gpu
 
 
-def _run(g: np.ndarray, K: int, r: int, q: int, mode: str, path: str):
+def _run(g: np.ndarray, K: int, r: int, q: int, mode: str, path: str, flags: int = 0):
     import torch
     gd = torch.from_numpy(np.ascontiguousarray(g)).to(device())
     if path == "entry_points":
@@ -28,15 +28,15 @@ def _run(g: np.ndarray, K: int, r: int, q: int, mode: str, path: str):
         torch.cuda.synchronize()
         return {"bufs": bufs, "clique": res, "out": out, "sel": sel, "n_selected": n,
                 "stats": {}}
-    flags = aspis.FLAG_TWO_PASS if path == "two_pass" else 0
+    flags |= aspis.FLAG_TWO_PASS if path == "two_pass" else 0
     got = aspis.detect_aggregate(gd, K, r, q, mode=mode, flags=flags | aspis.FLAG_TIMING)
     torch.cuda.synchronize()
     return got
 
 
-def _check(g, K, r, q, mode, path, nan_equal=False):
+def _check(g, K, r, q, mode, path, nan_equal=False, flags=0):
     ref = oracle.run(g, K, r, q, mode=mode)
-    got = _run(g, K, r, q, mode, path)
+    got = _run(g, K, r, q, mode, path, flags)
     assert_detection(got, ref, K)
     assert (to_np(got["sel"]) == ref["sel"]).all()
     assert got["n_selected"] == ref["n_selected"]
@@ -238,8 +238,11 @@ def test_random_half_key(seed):
     g, K, r, q = _random_half_case(seed)
     print(f"seed={seed} K={K} q={q} d={g.shape[2]}", flush=True)
     for path in ("fused", "two_pass"):
-        got, _ = _check(g, K, r, q, "median", path)
+        # the half-key tiles (forced: coarse values would send the tie
+        # probe to full keys), then whatever the tie probe picks
+        got, _ = _check(g, K, r, q, "median", path, flags=aspis.FLAG_HALF_KEYS)
         assert got["stats"]["half_keys"] == 1, got["stats"]
+        _check(g, K, r, q, "median", path)
 
 
 @pytest.mark.parametrize("K,r,d", [(26, 3, 301), (32, 3, 97), (9, 7, 333), (13, 5, 129),
@@ -305,8 +308,9 @@ def test_half_key_ties(K, q, d, kind):
     g, r = _ties_case(K, q, d, kind, seed=K * 1000 + d)
     print(f"K={K} q={q} d={d} kind={kind}", flush=True)
     for path in ("fused", "two_pass"):
-        got, ref = _check(g, K, r, q, "median", path, nan_equal=False)
+        got, ref = _check(g, K, r, q, "median", path, flags=aspis.FLAG_HALF_KEYS)
         assert got["stats"]["half_keys"] == 1, got["stats"]
+        auto, _ = _check(g, K, r, q, "median", path)   # the tie probe's choice
         assert ref["clique"]["success"]
 
 
