@@ -111,8 +111,11 @@ def cpu_baseline(torch, wl, chunk_of, d, gpu_out, gpu_sel, sample_coords: int, f
     res = oracle.run(g, K, r, q, mode=mode)
     dt1 = time.perf_counter() - t0
     slice_mean = mode == "mean" or (mode == "paper" and res["clique"]["success"])
-    parity_slice = bool(np.array_equal(res["sel"], gpu_sel)) and \
-        same(gpu_out[:n1], res["out"], slice_mean)
+    # comparable only where the slice alone detects what the whole vector
+    # does (an adversary that deviates only past the slice changes the
+    # selection): None otherwise; the full pass below checks every coordinate
+    parity_slice = (same(gpu_out[:n1], res["out"], slice_mean)
+                    if np.array_equal(res["sel"], gpu_sel) else None)
     single = {"value": round(g.nbytes / dt1 / 1e9, 4), "unit": "GB/s", "cores": 1,
               "seconds": round(dt1, 2),
               "sample": f"coordinates [0,{n1}) ({g.nbytes / 1e9:.2f} GB of replicas), one thread"}
@@ -257,9 +260,20 @@ def main() -> int:
                     help="skip the oracle over every coordinate on the host's threads")
     ap.add_argument("--adversary-late", type=int, default=0, metavar="P",
                     help="the adversaries send honest values on coordinates [0, P) and distort "
-                         "only after (Section 4.2's adversary, who knows the protocol): with P "
-                         "beyond the probed prefix every step's guess misses and the median is "
-                         "rerun (0 = off; 65536 is past any prefix)")
+                         "only after (Section 4.2's adversary, who knows the protocol): with the "
+                         "prefix probe (--probe prefix) and P past it every step's guess misses "
+                         "(0 = off; 65536 is past any prefix)")
+    ap.add_argument("--adversary-sparse", type=int, default=0, metavar="N",
+                    help="the adversaries send honest values everywhere but at N coordinates "
+                         "drawn (seeded) from [65536, d): a probe rarely sees them, and the "
+                         "guess misses (0 = off)")
+    ap.add_argument("--adversary-ids", choices=["seeded", "high"], default="seeded",
+                    help="which workers collude: the workload's seeded choice, or the q "
+                         "highest-numbered (with D the q lowest under Theorem 1's attack), so "
+                         "that an honest worker holds slot 0 of every distorted file")
+    ap.add_argument("--probe", choices=["spread", "prefix"], default="spread",
+                    help="the coordinates the guess is taken from: blocks drawn per call "
+                         "(default) or the prefix (ASPIS_FLAG_PROBE_PREFIX)")
     ap.add_argument("--simulate", action="store_true",
                     help="instead of the step, run the host distortion-fraction simulator over "
                          "the paper's tables (K=15, 21, 24), the K=50 sweep and the K=100, r=5 "
@@ -298,7 +312,9 @@ def main() -> int:
                                            "tied": synth.DIST_TIED}[args.dist])
     K, r, q, d, f = wl.K, wl.r, wl.q, wl.d, wl.f
     subsets = aspis.assign(K, r)
-    role, worker, A, D = synth.make_roles(wl, subsets, seed=args.seed)
+    ids = ({} if args.adversary_ids == "seeded" else
+           {"adversaries": list(range(K - q, K)), "disagree_set": list(range(q))})
+    role, worker, A, D = synth.make_roles(wl, subsets, seed=args.seed, **ids)
     t_gen = time.perf_counter()
     grads = torch.empty((f, r, d), dtype=torch.float32, device=dev)
     synth.fill_device(role, worker, grads, wl.dist, seed=args.seed, alie_z=wl.alie_z)
@@ -312,6 +328,19 @@ def main() -> int:
                           alie_z=wl.alie_z)
         grads[:, :, :P].copy_(clean)
         del clean
+    sparse = None
+    if args.adversary_sparse > 0:
+        # honest replicas everywhere, then the attack's values back at N
+        # coordinates past the longest probe prefix
+        lo = min(65536, d - 1)
+        sparse = sorted({lo + synth.u32(args.seed, 13, j) % (d - lo)
+                         for j in range(args.adversary_sparse)})
+        idx = torch.tensor(sparse, dtype=torch.int64, device=dev)
+        kept = grads.index_select(2, idx)
+        synth.fill_device(np.zeros_like(role), worker, grads, wl.dist, seed=args.seed,
+                          alie_z=wl.alie_z)
+        grads.index_copy_(2, idx, kept)
+        del kept, idx
     if args.layout == "worker":
         # the same replicas in the order the workers upload them
         l_files = f * r // K
@@ -331,7 +360,8 @@ def main() -> int:
     sel = torch.empty(f, dtype=torch.int32, device=dev)
     ws = aspis.workspace(K, r, d, dev)
     flags = (aspis.FLAG_TIMING | (aspis.FLAG_TWO_PASS if args.two_pass else 0)
-             | {"auto": 0, "half": aspis.FLAG_HALF_KEYS, "full": aspis.FLAG_FULL_KEYS}[args.keys])
+             | {"auto": 0, "half": aspis.FLAG_HALF_KEYS, "full": aspis.FLAG_FULL_KEYS}[args.keys]
+             | (aspis.FLAG_PROBE_PREFIX if args.probe == "prefix" else 0))
 
     def step():
         return aspis.detect_aggregate(grads, K, r, q, mode=args.mode, flags=flags, bufs=bufs,
@@ -382,14 +412,26 @@ def main() -> int:
         ceiling["step_frac"] = round(value / ceiling["GB/s"], 4)
 
     fallback = None
-    if last["fused"] and not last["speculation_hit"]:
-        ms_fb = float(np.mean([s["ms_fallback"] for s in stats]))
-        fb_bytes = step_out["n_selected"] * d * 4.0 + d * 4.0
-        fallback = {"kernel": f"{red} rerun over the final selection"
-                              + (f" ({last['tile_cols']}-column tiles)" if not by_mean else ""),
-                    "ms": round(ms_fb, 4), "algorithmic_bytes": fb_bytes,
-                    "achieved": round(fb_bytes / (ms_fb / 1e3) / 1e9, 1), "unit": "GB/s",
-                    "frac": round(fb_bytes / (ms_fb / 1e3) / 1e9 / HBM_PEAK_GBS, 4)}
+    missed = [s for s in stats if s["fused"] and not s["speculation_hit"]]
+    if missed:
+        # the reduction redone after the steps' wrong guesses: whole, or
+        # (same files, same median) the tile groups the moved files touch
+        ms_fb = float(np.mean([s["ms_fallback"] for s in missed]))
+        groups = [s["repair_groups"] for s in missed]
+        fallback = {"steps_missed": len(missed), "ms": round(ms_fb, 4),
+                    "repair_groups": groups[-1]}
+        if groups[-1] < 0:
+            fb_bytes = step_out["n_selected"] * d * 4.0 + d * 4.0
+            fallback.update({
+                "kernel": f"{red} rerun over the final selection"
+                          + (f" ({last['tile_cols']}-column tiles)" if not by_mean else ""),
+                "algorithmic_bytes": fb_bytes,
+                "achieved": round(fb_bytes / (ms_fb / 1e3) / 1e9, 1), "unit": "GB/s",
+                "frac": round(fb_bytes / (ms_fb / 1e3) / 1e9 / HBM_PEAK_GBS, 4)})
+        else:
+            fallback["kernel"] = ("dirty_tiles_kernel (moved files' two replicas compared) + "
+                                  f"median over the marked tile groups ({last['tile_cols']}-column "
+                                  "tiles)")
 
     cpu = None
     parity = {}
@@ -419,6 +461,9 @@ def main() -> int:
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
                    **({"adversary_late": min(args.adversary_late, d)}
                       if args.adversary_late > 0 else {}),
+                   **({"adversary_sparse": len(sparse)} if sparse else {}),
+                   **({"adversary_ids": args.adversary_ids}
+                      if args.adversary_ids != "seeded" else {}),
                    **({"dist": args.dist} if args.dist else {}),
                    "layout": "[f][r][d]" if args.layout == "file" else "[K][l][d] (worker uploads)",
                    "attack": wl.attack, "distortion": wl.distortion,
@@ -426,6 +471,10 @@ def main() -> int:
                    "replica_bytes": replica_bytes, "parallelism": "single GPU"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "path": {"fused": bool(last["fused"]), "speculation_hit": bool(last["speculation_hit"]),
+                 "steps_hit": sum(1 for s in stats if s["speculation_hit"]),
+                 "probe": args.probe, "probe_blocks": int(last["probe_blocks"]),
+                 "probe_coords": int(last["probe_coords"]),
+                 "repair_groups": int(last["repair_groups"]),
                  "ms_probe": round(last["ms_probe"], 4),
                  "ms_fallback": round(last["ms_fallback"], 4),
                  "tile_columns": int(last["tile_cols"]), "half_keys": bool(last["half_keys"]),

@@ -133,8 +133,10 @@ aspis_status aspis_clique(const uint64_t *disagree_rows, int32_t K, int32_t q,
 
 /* Bytes of workspace aspis_aggregate, aspis_detect_aggregate and
  * aspis_detect_aggregate_wm need: three int32 [f] arrays and one int32
- * [f*r] table, each rounded up to 256 bytes, plus 256 bytes of counters and
- * 1,024 bytes where the disagreement rows are staged for the host.
+ * [f*r] table, each rounded up to 256 bytes, 256 bytes of counters, 1,024
+ * bytes where the disagreement rows are staged for the host, and for the
+ * repair after a wrong guess an int8 [f] array rounded up to 256 bytes,
+ * 16,384 bytes of tile-group bits and 256 bytes of counters.
  * 0 on invalid arguments. */
 size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d);
 
@@ -163,9 +165,9 @@ aspis_status aspis_aggregate(const float *grads, int32_t K, int32_t r,
  * aspis_detect_aggregate. */
 typedef struct {
     int32_t fused;             /* 1 if the single-pass kernel ran           */
-    int32_t speculation_hit;   /* 1 if the prefix guess was confirmed       */
-    int64_t probe_coords;      /* coordinates in the probe prefix           */
-    float ms_probe;            /* prefix agreement pass                     */
+    int32_t speculation_hit;   /* 1 if the probe's guess was confirmed      */
+    int64_t probe_coords;      /* coordinates the guess was taken from      */
+    float ms_probe;            /* agreement pass over the probe             */
     float ms_main;             /* main pass (fused, or detect + reduce)     */
     float ms_fallback;         /* reduction rerun after a wrong guess       */
     float ms_total;            /* first kernel to result, host steps incl.  */
@@ -177,6 +179,14 @@ typedef struct {
                                   the median of the number of files whose
                                   value shares the high 16-bit key half of
                                   the files' median; -1 if not probed     */
+    int32_t probe_blocks;      /* blocks of 1,024 coordinates at positions
+                                  drawn per call; 0: the probe was the
+                                  prefix                                   */
+    int32_t repair_groups;     /* after a wrong guess that kept the same
+                                  files for the same median: the tile groups
+                                  recomputed (the others kept the guessed
+                                  median, already final there); -1 if the
+                                  step did not repair                      */
 } aspis_run_stats;
 
 #define ASPIS_FLAG_TWO_PASS 1u   /* force detect, clique, then aggregate    */
@@ -184,14 +194,24 @@ typedef struct {
 #define ASPIS_FLAG_FULL_KEYS 4u  /* median tiles of 32-bit keys only        */
 #define ASPIS_FLAG_HALF_KEYS 8u  /* half-key tiles wherever the plan has
                                     them, without the tie probe             */
+#define ASPIS_FLAG_PROBE_PREFIX 16u /* take the guess from the coordinate
+                                       prefix, not from blocks drawn per
+                                       call (reproducible speculation)      */
 
 /* The whole step in one call (Algorithm 3 then Algorithm 1): agreement,
  * host clique, selection and reduction, with the same outputs as
  * aspis_detect + aspis_clique + aspis_aggregate.  By default it reads the
- * replica tensor once: it guesses the selection from a short coordinate
- * prefix, reduces with that guess while checking agreement on all
- * coordinates, and reruns the reduction if the full detection disagrees
- * with the guess -- the result is exact either way.
+ * replica tensor once: it guesses the selection from a probe of a few
+ * thousand coordinates, reduces with that guess while checking agreement
+ * on all coordinates, and redoes the reduction if the full detection
+ * disagrees with the guess -- the result is exact either way.  The probe
+ * is the vector itself when d is at most its size, otherwise blocks of
+ * 1,024 coordinates at positions drawn per call (SplitMix64 of a random
+ * per-process seed and a call counter), so that a worker cannot know when
+ * it uploads which coordinates the guess reads; ASPIS_FLAG_PROBE_PREFIX
+ * takes the prefix instead.  After a wrong guess that kept the same files
+ * and asked for the same median, only the tiles holding a coordinate where
+ * some file's guessed and final replicas differ are recomputed.
  * Median tiles: the half-key tiles keep only the high 16 bits of each key
  * in LDS (twice the columns) and read back the low halves of the rows tied
  * with the median's high half.  Unless a key flag says otherwise, a tie
@@ -203,7 +223,7 @@ typedef struct {
  * Errors as aspis_aggregate's, except that on NO_FILES `out` holds no
  * result rather than being untouched: the single pass may have written it
  * with the guessed selection before the final one kept no file.
- * Synchronises the stream: twice on the single pass (the prefix graph and
+ * Synchronises the stream: twice on the single pass (the probe's graph and
  * the full graph), once more before returning. */
 aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
                                     int32_t q, int64_t d,
@@ -218,7 +238,8 @@ aspis_status aspis_detect_aggregate(const float *grads, int32_t K, int32_t r,
 /* For callers that cannot allocate (code under HIP graph capture, serving
  * loops and harnesses that forbid hipMalloc): aspis_detect_aggregate
  * without a workspace argument.  Its scratch (the selection, the kept-row
- * list, a counter and the staged disagreement rows) lives in a static
+ * list, counters, the staged disagreement rows and the repair's
+ * tile-group bits) lives in a static
  * device array of ASPIS_NOALLOC_SCRATCH_BYTES, one per device, held until
  * the process ends; its address is looked up on the first call on each
  * device.  The call allocates no device or host memory, and creates no

@@ -24,6 +24,7 @@ FLAG_TWO_PASS = 1
 FLAG_TIMING = 2
 FLAG_FULL_KEYS = 4
 FLAG_HALF_KEYS = 8
+FLAG_PROBE_PREFIX = 16
 
 EXPORTED = (
     "aspis_num_files", "aspis_assign", "aspis_detect", "aspis_clique",
@@ -81,7 +82,8 @@ class RunStats(ctypes.Structure):
                 ("probe_coords", ctypes.c_int64), ("ms_probe", ctypes.c_float),
                 ("ms_main", ctypes.c_float), ("ms_fallback", ctypes.c_float),
                 ("ms_total", ctypes.c_float), ("tile_cols", ctypes.c_int32),
-                ("half_keys", ctypes.c_int32), ("tie_rows", ctypes.c_int32)]
+                ("half_keys", ctypes.c_int32), ("tie_rows", ctypes.c_int32),
+                ("probe_blocks", ctypes.c_int32), ("repair_groups", ctypes.c_int32)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -3,11 +3,13 @@
 // orchestration of the gfx950 kernels (aspis_kernels.hip).
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <chrono>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <random>
 #include <vector>
 
 #include "../../include/aspis.h"
@@ -278,14 +280,42 @@ size_t aspis_aggregate_workspace(int32_t K, int32_t r, int64_t d) {
 
 namespace {
 
-// Coordinates of the prefix the single pass guesses its selection from:
-// about 2^24 replica words (200 MB; 0.3 % of the bytes at f = 455, d =
-// 11.2M), between 4,096 and 32,768 coordinates.  Any disagreement there is
-// caught; one that starts later only costs the rerun of the reduction.
+// Coordinates the single pass guesses its selection from: about 2^24
+// replica words (200 MB; 0.3 % of the bytes at f = 455, d = 11.2M), between
+// 4,096 and 32,768 coordinates.  Any disagreement there is caught; one
+// elsewhere only costs redoing the reduction (or the tiles it touches).
 int64_t probe_coords(int64_t f, int64_t d) {
     int64_t p = (int64_t(1) << 24) / (f > 0 ? f : 1);
     p = p < 4096 ? 4096 : p > 32768 ? 32768 : p;
     return d < p ? d : p;
+}
+
+// The seed of a probe drawn for this call: SplitMix64 of a per-process
+// random base and a call counter (never 0, which denotes the prefix).
+uint64_t probe_seed() {
+    static const uint64_t base = [] {
+        std::random_device rd;
+        return ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+    }();
+    static std::atomic<uint64_t> calls{0};
+    const uint64_t x = aspis::splitmix64(base + calls.fetch_add(1, std::memory_order_relaxed));
+    return x ? x : 1u;
+}
+
+// The probe of a call: the whole vector when d is no longer than the probe,
+// the prefix when asked, else blocks at positions drawn for the call.
+aspis::ProbeSet make_probe(int64_t f, int64_t d, uint32_t flags) {
+    const int64_t n = probe_coords(f, d);
+    aspis::ProbeSet p;
+    if (n >= d || (flags & ASPIS_FLAG_PROBE_PREFIX)) {
+        p.kend = n;
+        p.nb = (n + aspis::kProbeBlockCols - 1) / aspis::kProbeBlockCols;
+    } else {
+        p.nb = n / aspis::kProbeBlockCols;   // 4 to 32: n is 4,096 to 32,768 here
+        p.seed = probe_seed();
+        for (int64_t j = 0; j < p.nb; ++j) p.start[j] = aspis::probe_block_start(p.seed, j, d);
+    }
+    return p;
 }
 
 // The worker-major upload of Algorithm 1: worker u returns the gradients of
@@ -396,10 +426,12 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
     bool full_keys = (flags & ASPIS_FLAG_FULL_KEYS) != 0;
     const bool tie_probe =
         (flags & (ASPIS_FLAG_FULL_KEYS | ASPIS_FLAG_HALF_KEYS)) == 0 && mode != ASPIS_REDUCE_MEAN;
-    const int64_t probe = probe_coords(f, d);
-    const int n_tie = (int)(probe < aspis::kTieCols ? probe : aspis::kTieCols);
+    const aspis::ProbeSet probe = make_probe(f, d, flags);
+    const int n_tie = (int)(probe.coords() < aspis::kTieCols ? probe.coords() : aspis::kTieCols);
     uint32_t *tie_dev = reinterpret_cast<uint32_t *>(ws.stage + aspis::kStageTie);
     local.tie_rows = -1;
+    local.repair_groups = -1;
+    local.probe_blocks = probe.seed ? (int32_t)probe.nb : 0;
     auto decide_keys = [&](const uint64_t *staged_words) {
         if (!tie_probe) return;
         const uint32_t t = tie_estimate(
@@ -453,9 +485,9 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             ASPIS_HIP(hipStreamSynchronize(s));
             return aspis_clique(staged, K, q, out_res);
         };
-        // 1) agreement on a coordinate prefix -> provisional clique and
+        // 1) agreement on the probed coordinates -> provisional clique and
         //    selection; the tie probe rides on the same copy to the host
-        local.probe_coords = probe;
+        local.probe_coords = probe.coords();
         if (timing) ASPIS_HIP(hipEventRecord(ev[0], s));
         ASPIS_HIP(aspis::launch_agree_file(grads, row_of, f, r, d, probe, det->pair_diff, s));
         ASPIS_HIP(aspis::launch_vote_rows(det->pair_diff, subsets_dev, f, r, K, det->vote,
@@ -504,24 +536,39 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             const bool hit = same_sel && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
+            // a wrong guess that asked for the same median as the final
+            // detection is repaired tile by tile (every tile when the kept
+            // files differ): the guessed selection is saved for the compare
+            const bool repair = !hit && !guess_mean && !use_mean(mode, res);
+            if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
+            if (repair) ASPIS_HIP(aspis::launch_save_sel(ws, f, s));
             // the workspace describes the final selection from here on (the
             // rows and positions a rerun of the reduction reads)
             if (!hit || sel_out)
                 ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
                                                honest_mask(res), row_of, ws, sel_out, nullptr, 0,
                                                s));
-            if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
+            int32_t groups = -1;
             if (!hit) {
                 fused_tile = aspis::TileUse{};
-                if (use_mean(mode, res))
+                if (repair) {
+                    ASPIS_HIP(aspis::launch_dirty_tiles(grads, row_of, f, r, d, ws, det->pair_diff,
+                                                        full_keys, s));
+                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile, full_keys,
+                                                   true));
+                    ASPIS_HIP(hipMemcpyAsync(&groups, ws.repair, sizeof(int32_t),
+                                             hipMemcpyDeviceToHost, s));
+                } else if (use_mean(mode, res)) {
                     ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
-                else
+                } else {
                     ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile, full_keys));
+                }
             }
             local.tile_cols = fused_tile.cols;
             local.half_keys = fused_tile.half;
             if (timing) ASPIS_HIP(hipEventRecord(ev[5], s));
             ASPIS_HIP(hipStreamSynchronize(s));
+            local.repair_groups = groups;
             if (timing) {
                 ASPIS_HIP(hipEventElapsedTime(&local.ms_probe, ev[0], ev[1]));
                 ASPIS_HIP(hipEventElapsedTime(&local.ms_main, ev[2], ev[3]));

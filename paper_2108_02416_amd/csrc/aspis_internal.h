@@ -29,7 +29,13 @@ struct Workspace {
                       // [64] a vote-changed flag, [72,104) the tie probe's
                       // kTieCols uint32 counts (kStageTie)
     int32_t *row_of;  // [f*r] row of replica (i,s) in a worker-major upload
+    int8_t *sel_prev; // [f] the guessed selection's slots (repair after a miss)
+    uint32_t *dirty;  // [kDirtyWords] tile-group bits of the repair
+    int32_t *repair;  // [4] repair counters: [0] dirty tile groups
 };
+// Tile-group bits of the repair after a wrong guess: bit b covers tiles
+// [b*gran, (b+1)*gran), gran the least that fits every tile in these bits.
+constexpr int64_t kDirtyWords = 4096;
 constexpr int kStageTie = 72;      // first stage word of the tie counts
 constexpr int kStageWords = 104;   // stage words the host reads back
 size_t workspace_bytes(int64_t f, int r);
@@ -46,10 +52,46 @@ hipError_t launch_fill_u64(uint64_t *p, int64_t n, uint64_t v, hipStream_t s);
 hipError_t launch_agree(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                         int64_t k_end, uint32_t *pair_diff, hipStream_t s);
 
-// Agreement over coordinates [0, k_end) with one workgroup per file; stores
+// The coordinates the single pass guesses its selection from: nb blocks of
+// kProbeBlockCols coordinates.  seed == 0: the prefix [0, kend), in
+// consecutive blocks (the last one ends at kend).  Otherwise block j starts
+// at start[j], a multiple of kProbeAlign in [0, d - kProbeBlockCols] that
+// the host draws per call from a random seed (probe_block_start): a worker
+// cannot know when it uploads which coordinates the guess reads.
+constexpr int64_t kProbeBlockCols = 1024;
+constexpr int64_t kProbeAlign = 64;
+constexpr int kProbeMaxBlocks = 32;
+struct ProbeSet {
+    uint64_t seed = 0;   // 0: the prefix
+    int64_t nb = 0;      // blocks (<= kProbeMaxBlocks)
+    int64_t kend = 0;    // prefix: its end
+    int64_t start[kProbeMaxBlocks] = {};
+    int64_t coords() const { return seed ? nb * kProbeBlockCols : kend; }
+    __host__ __device__ int64_t block_start(int64_t j) const {
+        return seed ? start[j] : j * kProbeBlockCols;
+    }
+    __host__ __device__ int64_t block_end(int64_t b) const {
+        if (seed != 0) return b + kProbeBlockCols;
+        return b + kProbeBlockCols < kend ? b + kProbeBlockCols : kend;
+    }
+};
+// SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): the output function of
+// the generator, applied to the seed mixed with the block index.
+inline uint64_t splitmix64(uint64_t x) {
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+inline int64_t probe_block_start(uint64_t seed, int64_t j, int64_t d) {
+    const uint64_t slots = (uint64_t)((d - kProbeBlockCols) / kProbeAlign) + 1u;
+    return (int64_t)(splitmix64(seed ^ ((uint64_t)j << 32)) % slots) * kProbeAlign;
+}
+
+// Agreement over the probed coordinates with one workgroup per file; stores
 // every file's word (no zero fill needed).
 hipError_t launch_agree_file(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                             int64_t k_end, uint32_t *pair_diff, hipStream_t s);
+                             const ProbeSet &probe, uint32_t *pair_diff, hipStream_t s);
 
 // Per-file vote / majority flag and the disagreement rows (caller zeroes
 // disagree).
@@ -107,10 +149,12 @@ struct KernelPlan {
 bool plan_median(int64_t f, bool vec, KernelPlan *out, bool full_keys = false);
 bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out, bool full_keys = false);
 
-// Coordinate-wise lower median / fp64 mean of the kept rows.
+// Coordinate-wise lower median / fp64 mean of the kept rows.  With repair,
+// only the tiles of the groups ws.dirty marks (launch_dirty_tiles, same
+// f, d and full_keys) are computed; out keeps its values elsewhere.
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,
                          int64_t f, float *out, hipStream_t s, TileUse *use = nullptr,
-                         bool full_keys = false);
+                         bool full_keys = false, bool repair = false);
 hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
                        float *out, hipStream_t s);
 
@@ -135,13 +179,35 @@ bool fused_mean_supported(int64_t f, int r);
 constexpr size_t kScratchBytes = (size_t)2 << 20;
 hipError_t scratch_ptr(void **out);
 
-// Tie probe over coordinates [0, kend): for min(kTieCols, kend) coordinates
-// spread over them, out[j] = the number of files whose value (the value of
-// its largest class of equal replicas) shares the high 16-bit key half of
-// those values' lower median.  The host reads out[0 .. min(kTieCols, kend)).
+// Tie probe over the probed coordinates: for min(kTieCols, probe.coords())
+// coordinates spread over them, out[j] = the number of files whose value
+// (the value of its largest class of equal replicas) shares the high 16-bit
+// key half of those values' lower median.  The host reads that many words.
 constexpr int kTieCols = 64;
 hipError_t launch_tie_probe(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                            int64_t kend, uint32_t *out, hipStream_t s);
+                            const ProbeSet &probe, uint32_t *out, hipStream_t s);
+
+// Repair after a wrong guess whose selection kept the same files as the
+// final one (only the kept replica of some files moved) and whose reduction
+// was the same median: the guessed median is already the final one on
+// every coordinate where each moved file's two replicas are equal.
+// launch_save_sel copies ws.sel (the guess) to ws.sel_prev before the final
+// selection overwrites it, and zeroes the repair counters.
+// launch_dirty_tiles, after the final selection, marks in ws.dirty the tile
+// groups (tiles of the median plan launch_median takes for f, d and
+// full_keys) holding a coordinate where the replica of the guess and that of
+// the final selection of a moved file differ -- every group when the kept
+// files differ -- and counts them in ws.repair[0].  pair_diff: every file's
+// pair-difference bits over the whole vector.
+hipError_t launch_save_sel(const Workspace &ws, int64_t f, hipStream_t s);
+hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                              const Workspace &ws, const uint32_t *pair_diff, bool full_keys,
+                              hipStream_t s);
+// Tile groups: the bits' granularity for ntiles tiles.
+inline int64_t dirty_gran(int64_t ntiles) {
+    const int64_t bits = kDirtyWords * 32;
+    return ntiles <= bits ? 1 : (ntiles + bits - 1) / bits;
+}
 
 size_t read_probe_sink_words();
 hipError_t launch_read_probe(const void *buf, size_t nbytes, uint32_t *sink,

@@ -740,7 +740,8 @@ agree_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, in
 template <int R, bool VEC>
 __global__ void __launch_bounds__(kBlock)
 agree_file_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
-                  int64_t d, int64_t kend, uint32_t *__restrict__ pair_diff) {
+                  int64_t d, ProbeSet probe, uint32_t *__restrict__ pair_diff) {
+    static_assert(kProbeBlockCols == kBlock * 4, "one float4 per thread and probe block");
     __shared__ uint32_t wave_bits[kBlock / 64];
     constexpr int P = R * (R - 1) / 2;
     for (int64_t i = blockIdx.x; i < f; i += gridDim.x) {
@@ -748,11 +749,17 @@ agree_file_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_o
 #pragma unroll
         for (int s = 0; s < R; ++s) rows[s] = g + replica_row(row_of, i, R, s) * d;
         uint32_t diff = 0u;
-        for (int64_t k0 = 0; k0 < kend; k0 += kAgreeChunk) {
+        for (int64_t j0 = 0; j0 < probe.nb; j0 += kAgreeUnroll) {
             uint32_t v[kAgreeUnroll][R][4];
 #pragma unroll
             for (int u = 0; u < kAgreeUnroll; ++u) {
-                const int64_t k = k0 + (int64_t)u * kBlock * 4 + (int64_t)threadIdx.x * 4;
+                // block j0+u: the thread's four coordinates (none past its end)
+                int64_t k = 0, kend = 0;
+                if (j0 + u < probe.nb) {
+                    const int64_t b = probe.block_start(j0 + u);
+                    k = b + (int64_t)threadIdx.x * 4;
+                    kend = probe.block_end(b);
+                }
 #pragma unroll
                 for (int s = 0; s < R; ++s) {
                     if (k < kend)
@@ -938,11 +945,40 @@ select_kernel(const int32_t *__restrict__ subsets,
 
 constexpr int kMedianBatch = 8;   // row loads per thread issued as one burst
 
+// The tiles a median launch computes: every tile, or (a repair after a
+// wrong guess) the tiles of the groups whose bit is set, bit b for tiles
+// [b*gran, (b+1)*gran).  Uniform per workgroup.
+struct TileMask {
+    const uint32_t *bits = nullptr;
+    const int32_t *count = nullptr;   // groups set (no tile at all when 0)
+    int64_t gran = 1;
+    __device__ __forceinline__ bool has(int64_t t) const {
+        const int64_t b = t / gran;
+        return ((bits[b >> 5] >> (b & 31)) & 1u) != 0u;
+    }
+    // the first computed tile of t, t + step, ..., or one >= ntiles; the
+    // bits of eight candidates are read at once
+    __device__ __forceinline__ int64_t next(int64_t t, int64_t step, int64_t ntiles) const {
+        if (bits == nullptr) return t;
+        if (*count == 0) return ntiles;
+        for (; t < ntiles; t += 8 * step) {
+            uint32_t hit = 0u;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int64_t tu = t + u * step;
+                if (tu < ntiles && has(tu)) hit |= 1u << u;
+            }
+            if (hit) return t + (int64_t)(__ffs(hit) - 1) * step;
+        }
+        return ntiles;
+    }
+};
+
 template <int T, bool VEC>
 __global__ void __launch_bounds__(tile_block<T>())
 median_kernel(const float *__restrict__ g, int64_t d,
               const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
-              int64_t ntiles, float *__restrict__ out) {
+              int64_t ntiles, float *__restrict__ out, TileMask mask) {
     extern __shared__ uint32_t smem[];
     constexpr int BLOCK = tile_block<T>();
     uint32_t *hist = smem;
@@ -955,7 +991,8 @@ median_kernel(const float *__restrict__ g, int64_t d,
     const int tid = threadIdx.x;
     for (int i = tid; i < hist_words(T); i += BLOCK) hist[i] = 0u;
     const int cq = tid % CPR, j0 = tid / CPR;
-    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    for (int64_t t = mask.next(blockIdx.x, gridDim.x, ntiles); t < ntiles;
+         t = mask.next(t + gridDim.x, gridDim.x, ntiles)) {
         const int64_t k0 = t * T;
         for (int jb = 0; jb < n; jb += RPI * kMedianBatch) {
             uint32_t v[kMedianBatch][4];
@@ -1354,7 +1391,8 @@ constexpr int mws_batch() { return SW >= 16 ? 4 : (SW < 6 ? SW : 6); }
 template <int T, int SW, bool HALF, int FILL>
 __global__ void __launch_bounds__(kWsThreads)
 median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
-                 const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
+                 const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out,
+                 TileMask mask) {
     extern __shared__ uint32_t smem[];
     constexpr int G = (kWsThreads - FILL) / T;   // selection lanes per column
     constexpr int CPR = T / 4;           // float4 chunks per row segment
@@ -1437,25 +1475,31 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
                 }
             }
         };
-        int64_t t = blockIdx.x;
+        // the workgroup's tiles: t, then tn (whose sweep 0 is loaded early)
+        const int64_t G0 = gridDim.x;
+        int64_t t = mask.next(blockIdx.x, G0, ntiles);
+        int64_t tn = mask.next(t + G0, G0, ntiles);
         if (t < ntiles) {
             c0 = load_row(t, 0);
             stream_rest(t);
         }
-        if (t + gridDim.x < ntiles) c0 = load_row(t + gridDim.x, 0);
+        if (tn < ntiles) c0 = load_row(tn, 0);
         if (t < ntiles) put_tile();
         __syncthreads();
-        for (; t < ntiles; t += gridDim.x) {
-            const int64_t tn = t + gridDim.x;
+        while (t < ntiles) {
+            const int64_t tnn = mask.next(tn + G0, G0, ntiles);
             if (tn < ntiles) stream_rest(tn);
-            if (tn + gridDim.x < ntiles) c0 = load_row(tn + gridDim.x, 0);
+            if (tnn < ntiles) c0 = load_row(tnn, 0);
             __syncthreads();
             if (tn < ntiles) put_tile();
             __syncthreads();
+            t = tn;
+            tn = tnn;
         }
     } else {
         __syncthreads();
-        for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        for (int64_t t = mask.next(blockIdx.x, gridDim.x, ntiles); t < ntiles;
+             t = mask.next(t + gridDim.x, gridDim.x, ntiles)) {
             if constexpr (HALF) {
                 auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
                     return j < n ? (int64_t)rl[j] : -1;
@@ -1612,14 +1656,16 @@ constexpr int kRadixQuarter = kRadixBuckets / kRadixWaves;
 
 __global__ void __launch_bounds__(kRadixThreads)
 median_radix_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restrict__ rows,
-                    const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out) {
+                    const int32_t *__restrict__ n_sel, int64_t ntiles, float *__restrict__ out,
+                    TileMask mask) {
     __shared__ uint32_t hist[kRadixCols * kRadixStride];
     __shared__ uint32_t part[kRadixWaves][kRadixCols];   // bucket counts per quarter
     __shared__ uint32_t prefix[kRadixCols], rank[kRadixCols];
     const int n = *n_sel;
     if (n <= 0) return;   // uniform: no workgroup reaches a barrier
     const int tid = threadIdx.x, c = tid % kRadixCols, w = tid / kRadixCols;
-    for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    for (int64_t t = mask.next(blockIdx.x, gridDim.x, ntiles); t < ntiles;
+         t = mask.next(t + gridDim.x, gridDim.x, ntiles)) {
         const int64_t k = t * kRadixCols + c;
         const bool valid = k < d;
         if (tid < kRadixCols) {
@@ -1695,19 +1741,31 @@ median_radix_kernel(const float *__restrict__ g, int64_t d, const int32_t *__res
 // H.  It needs no selection, so it runs with the probe.
 
 constexpr int kTieThreads = 256;
+
+// Probed coordinate c (c < min(kTieCols, probe.coords())): the prefix
+// split in kTieCols equal steps, or offsets spread over the blocks.
+__device__ __forceinline__ int64_t tie_coord(const ProbeSet &probe, int c) {
+    if (probe.seed == 0) {
+        const int64_t kstep = probe.kend >= kTieCols ? probe.kend / kTieCols : 1;
+        return (int64_t)c * kstep;
+    }
+    const int64_t per = (kTieCols + probe.nb - 1) / probe.nb;   // coordinates per block
+    const int64_t step = kProbeBlockCols / per;
+    return probe.block_start(c % probe.nb) + (c / probe.nb) * step;
+}
 constexpr int kTieMaxFiles = 4096;   // files looked at per coordinate (the first ones)
 static_assert(kTieThreads == 256, "one histogram bucket per thread");
 
 template <int R>
 __global__ void __launch_bounds__(kTieThreads)
 tie_probe_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
-                 int64_t d, int64_t kstep, uint32_t *__restrict__ out) {
+                 int64_t d, ProbeSet probe, uint32_t *__restrict__ out) {
     __shared__ uint16_t h[kTieMaxFiles];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t wsum[kTieThreads / 64];
     __shared__ uint32_t pick[2];   // bucket, rank within it
     const int tid = threadIdx.x;
-    const int64_t k = (int64_t)blockIdx.x * kstep;   // < d (host)
+    const int64_t k = tie_coord(probe, blockIdx.x);
     const int n = (int)(f < kTieMaxFiles ? f : kTieMaxFiles);
     for (int i = tid; i < n; i += kTieThreads) {
         uint32_t v[R];
@@ -1767,6 +1825,116 @@ tie_probe_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of
             rank = pick[1];
         } else if (tid == 0) {
             out[blockIdx.x] = hist[b];
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// repair after a wrong guess (the guess kept the same files as the final
+// selection and reduced them with the same median): the median computed with
+// the guess already is the final one wherever each moved file's two
+// replicas are equal, so only the tiles holding a coordinate where they
+// differ are recomputed.
+
+__global__ void save_sel_kernel(const int32_t *__restrict__ sel, int64_t f,
+                                int8_t *__restrict__ sel_prev, int32_t *__restrict__ repair) {
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (i < f) sel_prev[i] = (int8_t)sel[i];
+    if (i < 4) repair[i] = 0;
+}
+
+constexpr int kDirtyMaxMoved = 2048;   // moved files a workgroup lists (LDS)
+constexpr int kDirtyBatch = 4;         // moved files per burst of loads
+
+// Every workgroup lists the moved files (replica rows of the guess and of the
+// final selection, where the two differ somewhere in the vector), then sets
+// the bits of its words: bit b of word w for the columns [b', b'+1) *
+// cols_per_bit, b' = 32w + b, when a listed pair differs there -- every bit
+// when the kept files differ or more files moved than the list holds.
+template <int R, bool VEC>
+__global__ void __launch_bounds__(kBlock)
+dirty_tiles_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
+                   int64_t d, int64_t cols_per_bit, int64_t nbits,
+                   const int8_t *__restrict__ sel_prev, const int32_t *__restrict__ sel,
+                   const uint32_t *__restrict__ pair_diff, uint32_t *__restrict__ dirty,
+                   int32_t *__restrict__ repair) {
+    __shared__ int32_t moved[2 * kDirtyMaxMoved];
+    __shared__ int32_t n_moved, every;
+    __shared__ uint32_t word;
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        n_moved = 0;
+        every = 0;
+        word = 0u;
+    }
+    __syncthreads();
+    for (int64_t i = tid; i < f; i += kBlock) {
+        const int a = sel_prev[i], b = sel[i];
+        if ((a < 0) != (b < 0)) {
+            atomicOr(&every, 1);
+            continue;
+        }
+        if (a < 0 || a == b) continue;
+        // bit of the slot pair (lo, hi) in the pair-difference word
+        const int lo = a < b ? a : b, hi = a < b ? b : a;
+        const int p = lo * (2 * R - lo - 1) / 2 + (hi - lo - 1);
+        if (((pair_diff[i] >> p) & 1u) == 0u) continue;   // bitwise equal replicas
+        const int x = atomicAdd(&n_moved, 1);
+        if (x < kDirtyMaxMoved) {
+            moved[2 * x] = (int32_t)replica_row(row_of, i, R, a);
+            moved[2 * x + 1] = (int32_t)replica_row(row_of, i, R, b);
+        } else {
+            atomicOr(&every, 1);
+        }
+    }
+    __syncthreads();
+    const bool all = every != 0;
+    const int n = n_moved < kDirtyMaxMoved ? n_moved : kDirtyMaxMoved;
+    const int64_t nwords = (nbits + 31) / 32;
+    for (int64_t w = blockIdx.x; w < nwords; w += gridDim.x) {
+        const int64_t nb = nbits - 32 * w < 32 ? nbits - 32 * w : 32;
+        const uint32_t full = nb == 32 ? 0xFFFFFFFFu : (1u << nb) - 1u;
+        if (all) {
+            if (tid == 0) {
+                dirty[w] = full;
+                atomicAdd(&repair[0], __popc(full));
+            }
+            continue;
+        }
+        const int64_t c0 = w * 32 * cols_per_bit;
+        const int64_t c1 = c0 + nb * cols_per_bit < d ? c0 + nb * cols_per_bit : d;
+        uint32_t mine = 0u;
+        for (int64_t k = c0 + 4 * tid; k < c1; k += 4 * kBlock) {
+            const uint32_t bit = 1u << ((k - c0) / cols_per_bit);
+            if (mine & bit) continue;
+            for (int x0 = 0; x0 < n; x0 += kDirtyBatch) {
+                uint32_t va[kDirtyBatch][4], vb[kDirtyBatch][4];
+#pragma unroll
+                for (int u = 0; u < kDirtyBatch; ++u) {
+                    if (x0 + u < n) {
+                        load4<VEC>(g + (int64_t)moved[2 * (x0 + u)] * d, k, d, va[u]);
+                        load4<VEC>(g + (int64_t)moved[2 * (x0 + u) + 1] * d, k, d, vb[u]);
+                    }
+                }
+                uint32_t diff = 0u;
+#pragma unroll
+                for (int u = 0; u < kDirtyBatch; ++u)
+                    if (x0 + u < n)
+                        diff |= (va[u][0] ^ vb[u][0]) | (va[u][1] ^ vb[u][1]) |
+                                (va[u][2] ^ vb[u][2]) | (va[u][3] ^ vb[u][3]);
+                if (diff != 0u) {
+                    mine |= bit;
+                    break;
+                }
+            }
+        }
+        if (mine) atomicOr(&word, mine);
+        __syncthreads();
+        if (tid == 0) {
+            dirty[w] = word;
+            atomicAdd(&repair[0], __popc(word));
+            word = 0u;
         }
         __syncthreads();
     }
@@ -1835,7 +2003,8 @@ constexpr size_t kWsCounters = 256, kWsStage = 1024;
 
 size_t workspace_bytes(int64_t f, int r) {
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return up((size_t)f * 4) * 3 + kWsCounters + kWsStage + up((size_t)f * r * 4);
+    return up((size_t)f * 4) * 3 + kWsCounters + kWsStage + up((size_t)f * r * 4) + up((size_t)f) +
+           (size_t)kDirtyWords * 4 + kWsCounters;
 }
 
 Workspace carve_workspace(void *base, int64_t f, int r) {
@@ -1853,7 +2022,12 @@ Workspace carve_workspace(void *base, int64_t f, int r) {
     w.stage = reinterpret_cast<uint64_t *>(p);
     p += kWsStage;
     w.row_of = reinterpret_cast<int32_t *>(p);
-    (void)r;   // the table holds f*r entries (workspace_bytes)
+    p += up((size_t)f * r * 4);
+    w.sel_prev = reinterpret_cast<int8_t *>(p);
+    p += up((size_t)f);
+    w.dirty = reinterpret_cast<uint32_t *>(p);
+    p += (size_t)kDirtyWords * 4;
+    w.repair = reinterpret_cast<int32_t *>(p);
     return w;
 }
 
@@ -1906,16 +2080,26 @@ hipError_t launch_vote_rows(const uint32_t *pair_diff, const int32_t *subsets, i
     return hipGetLastError();
 }
 
+// Every probed coordinate inside [0, d), the blocks within their count.
+bool probe_valid(const ProbeSet &p, int64_t d) {
+    if (p.nb <= 0 || p.nb > kProbeMaxBlocks) return false;
+    if (p.seed == 0) return p.kend > 0 && p.kend <= d && p.kend <= p.nb * kProbeBlockCols;
+    for (int64_t j = 0; j < p.nb; ++j)
+        if (p.start[j] < 0 || p.start[j] + kProbeBlockCols > d || p.start[j] % 4 != 0) return false;
+    return true;
+}
+
 hipError_t launch_agree_file(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                             int64_t kend, uint32_t *pair_diff, hipStream_t s) {
+                             const ProbeSet &probe, uint32_t *pair_diff, hipStream_t s) {
     if (f <= 0) return hipSuccess;
+    if (!probe_valid(probe, d)) return hipErrorInvalidValue;
     const unsigned grid = (unsigned)grid_for(f, (int64_t)num_cus() * 8);
     const bool vec = (d % 4 == 0) && aligned16(g);
-#define ASPIS_AGREE_FILE(RR)                                                                   \
-    if (vec)                                                                                   \
-        agree_file_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, pair_diff); \
-    else                                                                                       \
-        agree_file_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, kend, pair_diff);
+#define ASPIS_AGREE_FILE(RR)                                                                    \
+    if (vec)                                                                                    \
+        agree_file_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, probe, pair_diff); \
+    else                                                                                        \
+        agree_file_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, probe, pair_diff);
     switch (r) {
     case 3: ASPIS_AGREE_FILE(3) break;
     case 5: ASPIS_AGREE_FILE(5) break;
@@ -2108,7 +2292,7 @@ WsPlan ws_plan(int64_t f, int r, bool vec, bool ind, bool full_keys = false) {
 using FusedWsFn = void (*)(const float *, const int32_t *, int64_t, int64_t, const int32_t *,
                            const int32_t *, const int32_t *, int64_t, uint32_t *, float *);
 using MedianWsFn = void (*)(const float *, int64_t, const int32_t *, const int32_t *, int64_t,
-                            float *);
+                            float *, TileMask);
 
 FusedWsFn fused_ws_fn(const WsPlan &p, bool ind) {
     const int key = p.T * 1000 + p.sweeps * 10 + (p.half ? 1 : 0);
@@ -2319,23 +2503,30 @@ bool fused_supported(int64_t f, int r) {
 }
 
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t f,
-                         float *out, hipStream_t s, TileUse *use, bool full_keys) {
+                         float *out, hipStream_t s, TileUse *use, bool full_keys, bool repair) {
     const bool vec = (d % 4 == 0) && aligned16(g);
     KernelPlan k;
     if (!plan_median(f, vec, &k, full_keys)) return hipErrorInvalidValue;
     if (use) *use = TileUse{k.tile_cols, k.half_keys};
     const int T = k.tile_cols;
     const int64_t ntiles = (d + T - 1) / T;
+    TileMask mask;
+    if (repair) {
+        mask.bits = ws.dirty;
+        mask.count = ws.repair;
+        mask.gran = dirty_gran(ntiles);
+    }
     if (k.kind == kKernelMedianWs) {
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
         const MedianWsFn fn = median_ws_fn(mws_plan(f, vec, full_keys));
-        fn<<<grid, kWsThreads, (size_t)k.lds_bytes, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+        fn<<<grid, kWsThreads, (size_t)k.lds_bytes, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out, mask);
         return hipGetLastError();
     }
     if (k.kind == kKernelMedianRadix) {
         // LDS: 66 KB of histograms, two workgroups per CU
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus() * 2);
-        median_radix_kernel<<<grid, kRadixThreads, 0, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out);
+        median_radix_kernel<<<grid, kRadixThreads, 0, s>>>(g, d, ws.rows, ws.n_sel, ntiles, out,
+                                                           mask);
         return hipGetLastError();
     }
     const size_t lds = (size_t)k.lds_bytes;
@@ -2343,10 +2534,10 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
 #define ASPIS_MED(TT)                                                                        \
     if (vec)                                                                                 \
         median_kernel<TT, true><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
-                                                                   ntiles, out);             \
+                                                                   ntiles, out, mask);       \
     else                                                                                     \
         median_kernel<TT, false><<<grid, tile_block<TT>(), lds, s>>>(g, d, ws.rows, ws.n_sel, \
-                                                                    ntiles, out);
+                                                                    ntiles, out, mask);
     switch (T) {
     case 64: ASPIS_MED(64) break;
     case 32: ASPIS_MED(32) break;
@@ -2356,6 +2547,43 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     default: return hipErrorInvalidValue;
     }
 #undef ASPIS_MED
+    return hipGetLastError();
+}
+
+hipError_t launch_save_sel(const Workspace &ws, int64_t f, hipStream_t s) {
+    if (f <= 0) return hipErrorInvalidValue;
+    save_sel_kernel<<<(unsigned)((f + kBlock - 1) / kBlock), kBlock, 0, s>>>(ws.sel, f, ws.sel_prev,
+                                                                            ws.repair);
+    return hipGetLastError();
+}
+
+hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
+                              const Workspace &ws, const uint32_t *pair_diff, bool full_keys,
+                              hipStream_t s) {
+    const bool vec = (d % 4 == 0) && aligned16(g);
+    KernelPlan k;
+    if (f <= 0 || d <= 0 || !plan_median(f, vec, &k, full_keys)) return hipErrorInvalidValue;
+    const int64_t ntiles = (d + k.tile_cols - 1) / k.tile_cols;
+    const int64_t gran = dirty_gran(ntiles);
+    const int64_t nbits = (ntiles + gran - 1) / gran;
+    const int64_t cols_per_bit = gran * k.tile_cols;
+    const unsigned grid = (unsigned)grid_for((nbits + 31) / 32, (int64_t)num_cus() * 8);
+#define ASPIS_DIRTY(RR)                                                                         \
+    if (vec)                                                                                    \
+        dirty_tiles_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cols_per_bit,    \
+                                                             nbits, ws.sel_prev, ws.sel,       \
+                                                             pair_diff, ws.dirty, ws.repair);  \
+    else                                                                                        \
+        dirty_tiles_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cols_per_bit,   \
+                                                              nbits, ws.sel_prev, ws.sel,      \
+                                                              pair_diff, ws.dirty, ws.repair);
+    switch (r) {
+    case 3: ASPIS_DIRTY(3) break;
+    case 5: ASPIS_DIRTY(5) break;
+    case 7: ASPIS_DIRTY(7) break;
+    default: return hipErrorInvalidValue;
+    }
+#undef ASPIS_DIRTY
     return hipGetLastError();
 }
 
@@ -2475,14 +2703,14 @@ hipError_t scratch_ptr(void **out) {
 }
 
 hipError_t launch_tie_probe(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                            int64_t kend, uint32_t *out, hipStream_t s) {
-    if (f <= 0 || kend <= 0) return hipErrorInvalidValue;
-    const int64_t kstep = kend >= kTieCols ? kend / kTieCols : 1;
-    const unsigned grid = (unsigned)(kend >= kTieCols ? kTieCols : kend);
+                            const ProbeSet &probe, uint32_t *out, hipStream_t s) {
+    const int64_t n = probe.coords();
+    if (f <= 0 || n <= 0 || !probe_valid(probe, d)) return hipErrorInvalidValue;
+    const unsigned grid = (unsigned)(n >= kTieCols ? kTieCols : n);
     switch (r) {
-    case 3: tie_probe_kernel<3><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
-    case 5: tie_probe_kernel<5><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
-    case 7: tie_probe_kernel<7><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, kstep, out); break;
+    case 3: tie_probe_kernel<3><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, probe, out); break;
+    case 5: tie_probe_kernel<5><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, probe, out); break;
+    case 7: tie_probe_kernel<7><<<grid, kTieThreads, 0, s>>>(g, row_of, f, d, probe, out); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

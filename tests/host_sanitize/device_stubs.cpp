@@ -7,7 +7,9 @@
 
 namespace aspis {
 
-size_t workspace_bytes(int64_t f, int r) { return (size_t)f * 12 + 256 + 1024 + (size_t)f * r * 4 + 1024; }
+size_t workspace_bytes(int64_t f, int r) {
+    return (size_t)f * 12 + 256 + 1024 + (size_t)f * r * 4 + 1024 + (size_t)f + kDirtyWords * 4 + 256;
+}
 Workspace carve_workspace(void *, int64_t, int) { return Workspace{}; }
 hipError_t launch_fill_u32(uint32_t *, int64_t, uint32_t, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_fill_u64(uint64_t *, int64_t, uint64_t, hipStream_t) { return hipErrorInvalidValue; }
@@ -15,7 +17,7 @@ hipError_t launch_agree(const float *, const int32_t *, int64_t, int, int64_t, i
                         hipStream_t) {
     return hipErrorInvalidValue;
 }
-hipError_t launch_agree_file(const float *, const int32_t *, int64_t, int, int64_t, int64_t,
+hipError_t launch_agree_file(const float *, const int32_t *, int64_t, int, int64_t, const ProbeSet &,
                              uint32_t *, hipStream_t) {
     return hipErrorInvalidValue;
 }
@@ -42,7 +44,7 @@ bool plan_fused(int64_t, int, bool, bool, KernelPlan *out, bool) {
     return false;
 }
 hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, float *, hipStream_t,
-                         TileUse *, bool) {
+                         TileUse *, bool, bool) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_mean(const float *, int64_t, const Workspace &, float *, hipStream_t) {
@@ -59,8 +61,13 @@ hipError_t launch_fused_mean(const float *, const int32_t *, int64_t, int, int64
 }
 bool fused_mean_supported(int64_t, int) { return false; }
 hipError_t scratch_ptr(void **) { return hipErrorInvalidValue; }
-hipError_t launch_tie_probe(const float *, const int32_t *, int64_t, int, int64_t, int64_t,
+hipError_t launch_tie_probe(const float *, const int32_t *, int64_t, int, int64_t, const ProbeSet &,
                             uint32_t *, hipStream_t) {
+    return hipErrorInvalidValue;
+}
+hipError_t launch_save_sel(const Workspace &, int64_t, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t launch_dirty_tiles(const float *, const int32_t *, int64_t, int, int64_t, const Workspace &,
+                              const uint32_t *, bool, hipStream_t) {
     return hipErrorInvalidValue;
 }
 size_t read_probe_sink_words() { return 0; }

@@ -145,12 +145,14 @@ def test_worker_major_entry_validates_before_touching_the_gpu():
     assert call(16, 7, 3, 2, 10, ws=257) == aspis.ERR_INVALID_ARG  # unaligned workspace
     # the workspace of include/aspis.h: three int32 [f] arrays and the f*r
     # row table of the worker-major layout, each rounded up to 256 bytes,
-    # 256 bytes of counters and 1,024 of staged detection rows
+    # 256 bytes of counters and 1,024 of staged detection rows; the repair's
+    # int8 [f] array, 16,384 bytes of tile-group bits and 256 of counters
     def up(x):
         return (x + 255) // 256 * 256
     for K, r in ((7, 3), (15, 3), (25, 3), (9, 5), (9, 7)):
         f = comb(K, r)
-        assert L.aspis_aggregate_workspace(K, r, 10) == 3 * up(4 * f) + 256 + 1024 + up(4 * f * r)
+        assert L.aspis_aggregate_workspace(K, r, 10) == \
+            3 * up(4 * f) + 256 + 1024 + up(4 * f * r) + up(f) + 16384 + 256
 
 
 def test_read_probe_validates_before_touching_the_gpu():

@@ -99,9 +99,10 @@ def test_fused_mean_runs_single_pass(idx, mode):
 
 @pytest.mark.parametrize("mode", ["mean", "paper"])
 def test_fused_mean_guess_corrected(mode):
-    """A worker deviating only after the probe prefix: the mean computed with
-    the guessed selection is redone with the final one (PAPER also switches
-    from the mean to the median when detection fails in the end)."""
+    """A worker deviating only after the probe prefix (the prefix probe):
+    the mean computed with the guessed selection is redone with the final
+    one (PAPER also switches from the mean to the median when detection
+    fails in the end)."""
     wl = synth.WORKLOADS[1]
     s = oracle.assign(wl.K, wl.r)
     d = 65536 + 778
@@ -110,8 +111,9 @@ def test_fused_mean_guess_corrected(mode):
         for x in range(wl.r):
             if s[i, x] == 5:
                 g.view(np.uint32)[i, x, d - 5] ^= np.uint32(0x100)
-    got, _ = _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    got, _ = _check(g, wl.K, wl.r, wl.q, mode, "fused", flags=aspis.FLAG_PROBE_PREFIX)
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+    assert got["stats"]["repair_groups"] == -1   # a mean is redone whole
 
 
 def test_many_files_paper_mode():
@@ -336,9 +338,9 @@ def test_half_key_tile_widths(idx, path):
 
 
 def test_guess_from_prefix_is_wrong_then_corrected():
-    """The single-pass path guesses the selection from a prefix of at most
-    65,536 coordinates; a worker that deviates only after it makes the guess
-    wrong and the reduction must be redone with the final selection."""
+    """With the prefix probe (at most 32,768 coordinates), a worker that
+    deviates only after it makes the guess wrong and the reduction must be
+    redone with the final selection."""
     wl = synth.WORKLOADS[1]
     s = oracle.assign(wl.K, wl.r)
     d = 65536 + 777
@@ -348,7 +350,7 @@ def test_guess_from_prefix_is_wrong_then_corrected():
         for x in range(wl.r):
             if s[i, x] == 5:
                 g.view(np.uint32)[i, x, d - 3] ^= np.uint32(0x10)
-    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused")
+    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused", flags=aspis.FLAG_PROBE_PREFIX)
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
     assert not ref["clique"]["success"] or ref["clique"]["cliques"][0] != frozenset(range(2, 7))
 
@@ -372,13 +374,16 @@ def test_guess_miss_case2_vote_changes():
     assert (gb[i, 0] == gb[i, 1]).all() and (gb[i, 1] == gb[i, 2]).all()
     pre = oracle.detect(np.ascontiguousarray(g[:, :, :65536]), s, wl.K, wl.q)
     gb[i, 0, _LATE_D - 7] ^= np.uint32(0x40)
-    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused")
+    got, ref = _check(g, wl.K, wl.r, wl.q, "median", "fused", flags=aspis.FLAG_PROBE_PREFIX)
     # the path this test is about: same graph, same failed detection, one
     # file's vote moved from slot 0 to slot 1
     assert (pre["disagree"] == ref["disagree"]).all()
     assert not pre["clique"]["success"] and not ref["clique"]["success"]
     assert pre["vote"][i] == 0 and ref["vote"][i] == 1
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+    # every file kept either way, one file's replica moved: only the tile of
+    # the flipped coordinate is recomputed
+    assert got["stats"]["repair_groups"] == 1
 
 
 @pytest.mark.parametrize("mode", ["median", "paper"])
@@ -398,10 +403,16 @@ def test_guess_miss_case1_other_clique(mode):
             h = int(np.flatnonzero(s[i] >= 2)[0])   # a slot of an honest worker
             g[i, x, :d - 64] = g[i, h, :d - 64]
     pre = oracle.detect(np.ascontiguousarray(g[:, :, :65536]), s, wl.K, wl.q)
-    got, ref = _check(g, wl.K, wl.r, wl.q, mode, "fused")
+    got, ref = _check(g, wl.K, wl.r, wl.q, mode, "fused", flags=aspis.FLAG_PROBE_PREFIX)
     assert pre["clique"]["success"] and pre["clique"]["cliques"][0] == frozenset(range(1, 7))
     assert ref["clique"]["success"] and ref["clique"]["cliques"][0] == frozenset(range(2, 7))
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
+    # both keep every file (no file is held by workers 0 and 1 alone); the
+    # median is repaired on the tiles of the last 64 coordinates, the mean
+    # (PAPER: Case 1 both times) redone whole
+    T = got["stats"]["tile_cols"]
+    tiles = len({k // T for k in range(d - 64, d)}) if mode == "median" else -1
+    assert got["stats"]["repair_groups"] == tiles
 
 
 def test_guess_holds_on_clean_prefix():

@@ -131,9 +131,10 @@ def test_steady_state(name, spec, layout, flags, plan, ragged):
 
 def test_steady_state_guess_miss_rerun():
     """A guess miss at steady-state size: the headline workload with one
-    honest worker deviating past the probe prefix in every file it holds,
-    so the median of the single pass is redone by median_ws_kernel over the
-    final selection, with every workgroup on three or more tiles."""
+    honest worker deviating past the probe prefix (the prefix probe) in
+    every file it holds, so the median of the single pass is redone by
+    median_ws_kernel over the final selection, with every workgroup on three
+    or more tiles."""
     wl = synth.WORKLOADS[3]
     d = _steady_d(128, CUS, 36)
     s = oracle.assign(wl.K, wl.r)
@@ -141,7 +142,7 @@ def test_steady_state_guess_miss_rerun():
     fi, sl = np.nonzero(s == 9)
     g.view(np.uint32)[fi, sl, d - 11] ^= np.uint32(0x200)
     print(f"guess miss: d={d}", flush=True)
-    got = _run(g, wl.K, wl.r, wl.q)
+    got = _run(g, wl.K, wl.r, wl.q, flags=aspis.FLAG_PROBE_PREFIX)
     _compare(got, _oracle(g, wl.K, wl.r, wl.q, "median"), wl.K, "median")
     assert got["stats"]["fused"] == 1 and got["stats"]["speculation_hit"] == 0
 

@@ -87,8 +87,8 @@ def test_wider_files_worker_major(K, r, d):
 
 
 def test_guess_miss_worker_major():
-    """A worker deviating only after the probe prefix: the fallback runs
-    through the row table as well."""
+    """A worker deviating only after the probe prefix (the prefix probe):
+    the redone reduction runs through the row table as well."""
     wl = synth.WORKLOADS[1]
     s = oracle.assign(wl.K, wl.r)
     d = 65536 + 516
@@ -97,7 +97,7 @@ def test_guess_miss_worker_major():
         for x in range(wl.r):
             if s[i, x] == 5:
                 g.view(np.uint32)[i, x, d - 3] ^= np.uint32(0x10)
-    b, _ = _check(g, wl.K, wl.r, wl.q)
+    b, _ = _check(g, wl.K, wl.r, wl.q, flags=aspis.FLAG_PROBE_PREFIX)
     assert b["stats"]["fused"] == 1 and b["stats"]["speculation_hit"] == 0
 
 

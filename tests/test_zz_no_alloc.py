@@ -23,14 +23,15 @@ def _inputs(idx, d, seed=synth.SEED):
     return wl, torch.from_numpy(g).to(device())
 
 
-def _both(wl, gd, mode):
+def _both(wl, gd, mode, flags=0):
     import torch
     f, d = gd.shape[0], gd.shape[2]
-    ref = aspis.detect_aggregate(gd, wl.K, wl.r, wl.q, mode=mode)
+    ref = aspis.detect_aggregate(gd, wl.K, wl.r, wl.q, mode=mode, flags=flags)
     bufs = aspis.DetectBuffers.empty(f, wl.K, gd.device)
     out = torch.empty(d, dtype=torch.float32, device=gd.device)
     sel = torch.empty(f, dtype=torch.int32, device=gd.device)
-    got = aspis.detect_aggregate_noalloc(gd, wl.K, wl.r, wl.q, bufs, out, sel, mode=mode)
+    got = aspis.detect_aggregate_noalloc(gd, wl.K, wl.r, wl.q, bufs, out, sel, mode=mode,
+                                         flags=flags)
     torch.cuda.synchronize()
     return ref, got
 
@@ -42,7 +43,7 @@ def _same(ref, got, K):
     assert ref["n_selected"] == got["n_selected"]
     assert ref["clique"].as_dict(K) == got["clique"].as_dict(K)
     assert_same_floats(to_np(got["out"]), to_np(ref["out"]))
-    for k in ("fused", "speculation_hit", "tile_cols", "half_keys"):
+    for k in ("fused", "speculation_hit", "tile_cols", "half_keys", "repair_groups"):
         assert ref["stats"][k] == got["stats"][k], k
 
 
@@ -60,8 +61,10 @@ def test_noalloc_matches_workspace_entry_twice(mode):
 
 
 def test_noalloc_guess_miss_and_two_pass():
-    """The rerun after a wrong guess, and the two-pass path (flag), use the
-    same scratch for the selection and the kept-row list."""
+    """The redone reduction after a wrong guess (the prefix probe misses the
+    late deviation; the tiles it touches are repaired), and the two-pass
+    path (flag), use the same scratch for the selection and the kept-row
+    list."""
     import torch
     wl = synth.WORKLOADS[1]
     s = oracle.assign(wl.K, wl.r)
@@ -72,9 +75,9 @@ def test_noalloc_guess_miss_and_two_pass():
             if s[i, x] == 5:
                 g.view(np.uint32)[i, x, d - 3] ^= np.uint32(0x10)
     gd = torch.from_numpy(g).to(device())
-    ref, got = _both(wl, gd, "median")
+    ref, got = _both(wl, gd, "median", aspis.FLAG_PROBE_PREFIX)
     _same(ref, got, wl.K)
-    assert got["stats"]["speculation_hit"] == 0
+    assert got["stats"]["speculation_hit"] == 0 and got["stats"]["repair_groups"] >= 1
     bufs = aspis.DetectBuffers.empty(s.shape[0], wl.K, gd.device)
     out = torch.empty(d, dtype=torch.float32, device=gd.device)
     two = aspis.detect_aggregate_noalloc(gd, wl.K, wl.r, wl.q, bufs, out,
