@@ -34,7 +34,7 @@ struct Workspace {
     int32_t *repair;  // [4] repair counters: [0] dirty tile groups
 };
 // Tile-group bits of the repair after a wrong guess: bit b covers tiles
-// [b*gran, (b+1)*gran), gran the least that fits every tile in these bits.
+// [b << s, (b + 1) << s), s the least that fits every tile in these bits.
 constexpr int64_t kDirtyWords = 4096;
 constexpr int kStageTie = 72;      // first stage word of the tie counts
 constexpr int kStageWords = 104;   // stage words the host reads back
@@ -203,10 +203,12 @@ hipError_t launch_save_sel(const Workspace &ws, int64_t f, hipStream_t s);
 hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
                               const Workspace &ws, const uint32_t *pair_diff, bool full_keys,
                               hipStream_t s);
-// Tile groups: the bits' granularity for ntiles tiles.
-inline int64_t dirty_gran(int64_t ntiles) {
-    const int64_t bits = kDirtyWords * 32;
-    return ntiles <= bits ? 1 : (ntiles + bits - 1) / bits;
+// Tile groups: 2^shift tiles a bit, the least power of two that fits
+// ntiles tiles in the bits.
+inline int dirty_gran_shift(int64_t ntiles) {
+    int sh = 0;
+    while (((ntiles + (int64_t(1) << sh) - 1) >> sh) > kDirtyWords * 32) ++sh;
+    return sh;
 }
 
 size_t read_probe_sink_words();

@@ -947,21 +947,22 @@ constexpr int kMedianBatch = 8;   // row loads per thread issued as one burst
 
 // The tiles a median launch computes: every tile, or (a repair after a
 // wrong guess) the tiles of the groups whose bit is set, bit b for tiles
-// [b*gran, (b+1)*gran).  Uniform per workgroup.
+// [b << gshift, (b + 1) << gshift).  Uniform per workgroup.
 struct TileMask {
     const uint32_t *bits = nullptr;
     const int32_t *count = nullptr;   // groups set (no tile at all when 0)
-    int64_t gran = 1;
+    int gshift = 0;
     __device__ __forceinline__ bool has(int64_t t) const {
-        const int64_t b = t / gran;
+        const int64_t b = t >> gshift;
         return ((bits[b >> 5] >> (b & 31)) & 1u) != 0u;
     }
-    // the first computed tile of t, t + step, ..., or one >= ntiles; the
-    // bits of eight candidates are read at once
+    // the first computed tile of t, t + step, ..., or one >= ntiles: t
+    // itself when its bit is set, else the bits of eight candidates at once
     __device__ __forceinline__ int64_t next(int64_t t, int64_t step, int64_t ntiles) const {
-        if (bits == nullptr) return t;
+        if (bits == nullptr || t >= ntiles) return t;
         if (*count == 0) return ntiles;
-        for (; t < ntiles; t += 8 * step) {
+        if (has(t)) return t;
+        for (t += step; t < ntiles; t += 8 * step) {
             uint32_t hit = 0u;
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
@@ -1849,13 +1850,14 @@ constexpr int kDirtyBatch = 4;         // moved files per burst of loads
 
 // Every workgroup lists the moved files (replica rows of the guess and of the
 // final selection, where the two differ somewhere in the vector), then sets
-// the bits of its words: bit b of word w for the columns [b', b'+1) *
-// cols_per_bit, b' = 32w + b, when a listed pair differs there -- every bit
-// when the kept files differ or more files moved than the list holds.
+// the bits of its words: bit b of word w for the columns [b' << cshift,
+// (b' + 1) << cshift), b' = 32w + b, when a listed pair differs there --
+// every bit when the kept files differ or more files moved than the list
+// holds.
 template <int R, bool VEC>
 __global__ void __launch_bounds__(kBlock)
 dirty_tiles_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_of, int64_t f,
-                   int64_t d, int64_t cols_per_bit, int64_t nbits,
+                   int64_t d, int cshift, int64_t nbits,
                    const int8_t *__restrict__ sel_prev, const int32_t *__restrict__ sel,
                    const uint32_t *__restrict__ pair_diff, uint32_t *__restrict__ dirty,
                    int32_t *__restrict__ repair) {
@@ -1902,11 +1904,11 @@ dirty_tiles_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_
             }
             continue;
         }
-        const int64_t c0 = w * 32 * cols_per_bit;
-        const int64_t c1 = c0 + nb * cols_per_bit < d ? c0 + nb * cols_per_bit : d;
+        const int64_t c0 = (w * 32) << cshift;
+        const int64_t c1 = c0 + (nb << cshift) < d ? c0 + (nb << cshift) : d;
         uint32_t mine = 0u;
         for (int64_t k = c0 + 4 * tid; k < c1; k += 4 * kBlock) {
-            const uint32_t bit = 1u << ((k - c0) / cols_per_bit);
+            const uint32_t bit = 1u << ((k - c0) >> cshift);
             if (mine & bit) continue;
             for (int x0 = 0; x0 < n; x0 += kDirtyBatch) {
                 uint32_t va[kDirtyBatch][4], vb[kDirtyBatch][4];
@@ -2514,7 +2516,7 @@ hipError_t launch_median(const float *g, int64_t d, const Workspace &ws, int64_t
     if (repair) {
         mask.bits = ws.dirty;
         mask.count = ws.repair;
-        mask.gran = dirty_gran(ntiles);
+        mask.gshift = dirty_gran_shift(ntiles);
     }
     if (k.kind == kKernelMedianWs) {
         const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus());
@@ -2564,17 +2566,19 @@ hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, 
     KernelPlan k;
     if (f <= 0 || d <= 0 || !plan_median(f, vec, &k, full_keys)) return hipErrorInvalidValue;
     const int64_t ntiles = (d + k.tile_cols - 1) / k.tile_cols;
-    const int64_t gran = dirty_gran(ntiles);
-    const int64_t nbits = (ntiles + gran - 1) / gran;
-    const int64_t cols_per_bit = gran * k.tile_cols;
+    const int gshift = dirty_gran_shift(ntiles);
+    const int64_t nbits = (ntiles + (int64_t(1) << gshift) - 1) >> gshift;
+    int cshift = gshift;   // columns per bit: tile_cols << gshift (tile_cols a power of two)
+    for (int c = k.tile_cols; c > 1; c >>= 1) ++cshift;
+    if ((int64_t(1) << (cshift - gshift)) != k.tile_cols) return hipErrorInvalidValue;
     const unsigned grid = (unsigned)grid_for((nbits + 31) / 32, (int64_t)num_cus() * 8);
 #define ASPIS_DIRTY(RR)                                                                         \
     if (vec)                                                                                    \
-        dirty_tiles_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cols_per_bit,    \
+        dirty_tiles_kernel<RR, true><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cshift,          \
                                                              nbits, ws.sel_prev, ws.sel,       \
                                                              pair_diff, ws.dirty, ws.repair);  \
     else                                                                                        \
-        dirty_tiles_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cols_per_bit,   \
+        dirty_tiles_kernel<RR, false><<<grid, kBlock, 0, s>>>(g, row_of, f, d, cshift,         \
                                                               nbits, ws.sel_prev, ws.sel,      \
                                                               pair_diff, ws.dirty, ws.repair);
     switch (r) {

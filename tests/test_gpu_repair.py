@@ -44,24 +44,40 @@ def _attack_only_at(wl, s, d, coords, seed=synth.SEED, **role_kw):
     return g
 
 
+GROUP_BITS = 4096 * 32   # tile-group bits of the repair
+
+
+def _group_shift(ntiles):
+    """Tiles per group: the least power of two 2^s with ceil(ntiles / 2^s)
+    groups fitting the bits."""
+    s = 0
+    while -(-ntiles // (1 << s)) > GROUP_BITS:
+        s += 1
+    return s
+
+
+def _groups_of(cols, T, d):
+    sh = _group_shift((d + T - 1) // T)
+    return len({(c // T) >> sh for c in cols})
+
+
 def _expected_groups(g, s, K, q, ref, T):
-    """Tile groups (one tile each at these sizes) the repair recomputes:
-    every tile when the prefix guess keeps other files than the final
-    selection, else the tiles where a moved file's two replicas differ."""
+    """Tile groups the repair recomputes: every group when the prefix guess
+    keeps other files than the final selection, else the groups holding a
+    coordinate where a moved file's two replicas differ."""
     f, r, d = g.shape
     ntiles = (d + T - 1) // T
-    assert ntiles <= 4096 * 32
     pre = oracle.detect(np.ascontiguousarray(g[:, :, :_probe(f, d)]), s, K, q)
     cl = pre["clique"]
     guess, _ = oracle.select(s, pre["vote"], cl["success"], cl["honest"])
     final = ref["sel"]
     if ((guess < 0) != (final < 0)).any():
-        return ntiles
+        return -(-ntiles // (1 << _group_shift(ntiles)))
     bits = g.view(np.uint32)
     cols = np.zeros(d, dtype=bool)
     for i in np.flatnonzero((guess >= 0) & (guess != final)):
         cols |= bits[i, guess[i]] != bits[i, final[i]]
-    return len(set((np.flatnonzero(cols) // T).tolist()))
+    return _groups_of(np.flatnonzero(cols).tolist(), T, d)
 
 
 def _coords(f, d):
@@ -189,3 +205,21 @@ def test_repair_five_replicas():
     print(f"r=5 sparse deviation: d={d}", flush=True)
     got, _, want = _repaired(g, K, r, q)
     assert want == len({c // got["stats"]["tile_cols"] for c in coords}) == 3
+
+
+def test_repair_groups_of_two_tiles():
+    """More tiles than group bits (133K tiles of 64 columns at K = 7): each
+    bit covers two tiles, and the three groups of four deviating
+    coordinates are recomputed."""
+    wl, kw = _late_workload(7, 3, 2)
+    K, r, q = wl.K, wl.r, wl.q
+    d = 64 * (GROUP_BITS + 1700) + 36
+    s = oracle.assign(K, r)
+    coords = _coords(wl.f, d)
+    g = _attack_only_at(wl, s, d, coords, **kw)
+    print(f"groups of two tiles: d={d}", flush=True)
+    got, ref, want = _repaired(g, K, r, q)
+    assert not ref["clique"]["success"] and ref["n_selected"] == comb(K, r)
+    T = got["stats"]["tile_cols"]
+    assert T == 64 and _group_shift((d + T - 1) // T) == 1
+    assert want == _groups_of(coords, T, d) == 3
