@@ -429,9 +429,9 @@ def main() -> int:
                 "achieved": round(fb_bytes / (ms_fb / 1e3) / 1e9, 1), "unit": "GB/s",
                 "frac": round(fb_bytes / (ms_fb / 1e3) / 1e9 / HBM_PEAK_GBS, 4)})
         else:
+            tiles = "1024-column" if by_mean else f"{last['tile_cols']}-column"
             fallback["kernel"] = ("dirty_tiles_kernel (moved files' two replicas compared) + "
-                                  f"median over the marked tile groups ({last['tile_cols']}-column "
-                                  "tiles)")
+                                  f"{red} over the marked tile groups ({tiles} tiles)")
 
     cpu = None
     parity = {}

@@ -536,10 +536,11 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             const bool hit = same_sel && use_mean(mode, res) == guess_mean;
             local.speculation_hit = hit ? 1 : 0;
             if (m == 0) return fail(ASPIS_ERR_NO_FILES, "selection kept no file");
-            // a wrong guess that asked for the same median as the final
+            // a wrong guess that asked for the same reduction as the final
             // detection is repaired tile by tile (every tile when the kept
             // files differ): the guessed selection is saved for the compare
-            const bool repair = !hit && !guess_mean && !use_mean(mode, res);
+            const bool final_mean = use_mean(mode, res);
+            const bool repair = !hit && guess_mean == final_mean;
             if (timing) ASPIS_HIP(hipEventRecord(ev[4], s));
             if (repair) ASPIS_HIP(aspis::launch_save_sel(ws, f, s));
             // the workspace describes the final selection from here on (the
@@ -552,13 +553,17 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
             if (!hit) {
                 fused_tile = aspis::TileUse{};
                 if (repair) {
+                    const int cols = aspis::reduce_tile_cols(grads, f, d, final_mean, full_keys);
                     ASPIS_HIP(aspis::launch_dirty_tiles(grads, row_of, f, r, d, ws, det->pair_diff,
-                                                        full_keys, s));
-                    ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile, full_keys,
-                                                   true));
+                                                        cols, s));
+                    if (final_mean)
+                        ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s, true));
+                    else
+                        ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile,
+                                                       full_keys, true));
                     ASPIS_HIP(hipMemcpyAsync(&groups, ws.repair, sizeof(int32_t),
                                              hipMemcpyDeviceToHost, s));
-                } else if (use_mean(mode, res)) {
+                } else if (final_mean) {
                     ASPIS_HIP(aspis::launch_mean(grads, d, ws, out, s));
                 } else {
                     ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile, full_keys));

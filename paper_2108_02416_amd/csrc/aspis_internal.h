@@ -150,13 +150,13 @@ bool plan_median(int64_t f, bool vec, KernelPlan *out, bool full_keys = false);
 bool plan_fused(int64_t f, int r, bool vec, bool ind, KernelPlan *out, bool full_keys = false);
 
 // Coordinate-wise lower median / fp64 mean of the kept rows.  With repair,
-// only the tiles of the groups ws.dirty marks (launch_dirty_tiles, same
-// f, d and full_keys) are computed; out keeps its values elsewhere.
+// only the tiles of the groups ws.dirty marks (launch_dirty_tiles with the
+// launch's reduce_tile_cols) are computed; out keeps its values elsewhere.
 hipError_t launch_median(const float *g, int64_t d, const Workspace &ws,
                          int64_t f, float *out, hipStream_t s, TileUse *use = nullptr,
                          bool full_keys = false, bool repair = false);
 hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws,
-                       float *out, hipStream_t s);
+                       float *out, hipStream_t s, bool repair = false);
 
 // Single pass: agreement bits of every file over [0, d) and the median of
 // the rows selected by ws (a guess), in one read of the replica tensor.
@@ -189,20 +189,24 @@ hipError_t launch_tie_probe(const float *g, const int32_t *row_of, int64_t f, in
 
 // Repair after a wrong guess whose selection kept the same files as the
 // final one (only the kept replica of some files moved) and whose reduction
-// was the same median: the guessed median is already the final one on
-// every coordinate where each moved file's two replicas are equal.
+// was the same (the median, or the mean, summed in file order either way):
+// the guessed result is already the final one on every coordinate where
+// each moved file's two replicas are equal.
 // launch_save_sel copies ws.sel (the guess) to ws.sel_prev before the final
 // selection overwrites it, and zeroes the repair counters.
 // launch_dirty_tiles, after the final selection, marks in ws.dirty the tile
-// groups (tiles of the median plan launch_median takes for f, d and
-// full_keys) holding a coordinate where the replica of the guess and that of
+// groups (tiles of tile_cols coordinates: reduce_tile_cols of the repairing
+// launch) holding a coordinate where the replica of the guess and that of
 // the final selection of a moved file differ -- every group when the kept
 // files differ -- and counts them in ws.repair[0].  pair_diff: every file's
 // pair-difference bits over the whole vector.
 hipError_t launch_save_sel(const Workspace &ws, int64_t f, hipStream_t s);
 hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                              const Workspace &ws, const uint32_t *pair_diff, bool full_keys,
+                              const Workspace &ws, const uint32_t *pair_diff, int tile_cols,
                               hipStream_t s);
+// Coordinates per tile of launch_mean (mean) or launch_median (f kept rows,
+// full_keys) on g: the tile width of their repair.
+int reduce_tile_cols(const float *g, int64_t f, int64_t d, bool mean, bool full_keys);
 // Tile groups: 2^shift tiles a bit, the least power of two that fits
 // ntiles tiles in the bits.
 inline int dirty_gran_shift(int64_t ntiles) {

@@ -1605,18 +1605,21 @@ fused_mean_kernel(const float *__restrict__ g, const int32_t *__restrict__ row_o
 // mean of the kept rows (fp64, file order)
 
 constexpr int kMeanRows = 8;
+constexpr int64_t kMeanTileCols = kBlock * 4;   // coordinates per mean tile: four per thread
 
 template <bool VEC>
 __global__ void __launch_bounds__(kBlock)
 mean_kernel(const float *__restrict__ g, int64_t d,
             const int32_t *__restrict__ rows, const int32_t *__restrict__ n_sel,
-            float *__restrict__ out) {
+            float *__restrict__ out, TileMask mask) {
     const int n = *n_sel;
     if (n <= 0) return;
-    const int64_t nquads = (d + 3) / 4;
-    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nquads;
-         q += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = q * 4;
+    // tiles of kMeanTileCols coordinates, four per thread
+    const int64_t ntiles = (d + kMeanTileCols - 1) / kMeanTileCols;
+    for (int64_t t = mask.next(blockIdx.x, gridDim.x, ntiles); t < ntiles;
+         t = mask.next(t + gridDim.x, gridDim.x, ntiles)) {
+        const int64_t k = t * kMeanTileCols + 4 * (int64_t)threadIdx.x;
+        if (k >= d) continue;
         double acc[4] = {0.0, 0.0, 0.0, 0.0};
         // bursts of kMeanRows loads, then the additions in row order
         for (int j0 = 0; j0 < n; j0 += kMeanRows) {
@@ -2560,17 +2563,16 @@ hipError_t launch_save_sel(const Workspace &ws, int64_t f, hipStream_t s) {
 }
 
 hipError_t launch_dirty_tiles(const float *g, const int32_t *row_of, int64_t f, int r, int64_t d,
-                              const Workspace &ws, const uint32_t *pair_diff, bool full_keys,
+                              const Workspace &ws, const uint32_t *pair_diff, int tile_cols,
                               hipStream_t s) {
     const bool vec = (d % 4 == 0) && aligned16(g);
-    KernelPlan k;
-    if (f <= 0 || d <= 0 || !plan_median(f, vec, &k, full_keys)) return hipErrorInvalidValue;
-    const int64_t ntiles = (d + k.tile_cols - 1) / k.tile_cols;
+    if (f <= 0 || d <= 0 || tile_cols < 4 || (tile_cols & (tile_cols - 1)) != 0)
+        return hipErrorInvalidValue;
+    const int64_t ntiles = (d + tile_cols - 1) / tile_cols;
     const int gshift = dirty_gran_shift(ntiles);
     const int64_t nbits = (ntiles + (int64_t(1) << gshift) - 1) >> gshift;
-    int cshift = gshift;   // columns per bit: tile_cols << gshift (tile_cols a power of two)
-    for (int c = k.tile_cols; c > 1; c >>= 1) ++cshift;
-    if ((int64_t(1) << (cshift - gshift)) != k.tile_cols) return hipErrorInvalidValue;
+    int cshift = gshift;   // columns per bit: tile_cols << gshift
+    for (int c = tile_cols; c > 1; c >>= 1) ++cshift;
     const unsigned grid = (unsigned)grid_for((nbits + 31) / 32, (int64_t)num_cus() * 8);
 #define ASPIS_DIRTY(RR)                                                                         \
     if (vec)                                                                                    \
@@ -2670,14 +2672,27 @@ hipError_t launch_fused_mean(const float *g, const int32_t *row_of, int64_t f, i
 }
 
 hipError_t launch_mean(const float *g, int64_t d, const Workspace &ws, float *out,
-                       hipStream_t s) {
-    const int64_t nquads = (d + 3) / 4;
-    const unsigned grid = (unsigned)grid_for((nquads + kBlock - 1) / kBlock, (int64_t)num_cus() * 8);
+                       hipStream_t s, bool repair) {
+    const int64_t ntiles = (d + kMeanTileCols - 1) / kMeanTileCols;
+    const unsigned grid = (unsigned)grid_for(ntiles, (int64_t)num_cus() * 8);
+    TileMask mask;
+    if (repair) {
+        mask.bits = ws.dirty;
+        mask.count = ws.repair;
+        mask.gshift = dirty_gran_shift(ntiles);
+    }
     if ((d % 4 == 0) && aligned16(g))
-        mean_kernel<true><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out);
+        mean_kernel<true><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out, mask);
     else
-        mean_kernel<false><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out);
+        mean_kernel<false><<<grid, kBlock, 0, s>>>(g, d, ws.rows, ws.n_sel, out, mask);
     return hipGetLastError();
+}
+
+int reduce_tile_cols(const float *g, int64_t f, int64_t d, bool mean, bool full_keys) {
+    if (mean) return (int)kMeanTileCols;
+    KernelPlan k;
+    const bool vec = (d % 4 == 0) && aligned16(g);
+    return plan_median(f, vec, &k, full_keys) ? k.tile_cols : 0;
 }
 
 // The workspace of the allocation-free entry point: a static device array,

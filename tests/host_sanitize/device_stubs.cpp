@@ -47,7 +47,7 @@ hipError_t launch_median(const float *, int64_t, const Workspace &, int64_t, flo
                          TileUse *, bool, bool) {
     return hipErrorInvalidValue;
 }
-hipError_t launch_mean(const float *, int64_t, const Workspace &, float *, hipStream_t) {
+hipError_t launch_mean(const float *, int64_t, const Workspace &, float *, hipStream_t, bool) {
     return hipErrorInvalidValue;
 }
 hipError_t launch_fused(const float *, const int32_t *, int64_t, int, int64_t, const Workspace &,
@@ -67,9 +67,10 @@ hipError_t launch_tie_probe(const float *, const int32_t *, int64_t, int, int64_
 }
 hipError_t launch_save_sel(const Workspace &, int64_t, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_dirty_tiles(const float *, const int32_t *, int64_t, int, int64_t, const Workspace &,
-                              const uint32_t *, bool, hipStream_t) {
+                              const uint32_t *, int, hipStream_t) {
     return hipErrorInvalidValue;
 }
+int reduce_tile_cols(const float *, int64_t, int64_t, bool, bool) { return 0; }
 size_t read_probe_sink_words() { return 0; }
 hipError_t launch_read_probe(const void *, size_t, uint32_t *, hipStream_t) {
     return hipErrorInvalidValue;

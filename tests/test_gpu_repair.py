@@ -96,14 +96,19 @@ def _late_workload(K, r, q):
     return wl, dict(adversaries=list(range(K - q, K)), disagree_set=list(range(q)))
 
 
-def _repaired(g, K, r, q, layout="file"):
+MEAN_TILE = 1024   # coordinates per tile of the mean kernel
+
+
+def _repaired(g, K, r, q, layout="file", mode="median"):
     s = oracle.assign(K, r)
-    ref = _oracle(g, K, r, q, "median")
-    got = _run(g, K, r, q, flags=PREFIX, layout=layout)
-    _compare(got, ref, K, "median")
+    ref = _oracle(g, K, r, q, mode)
+    got = _run(g, K, r, q, mode=mode, flags=PREFIX, layout=layout)
+    _compare(got, ref, K, mode)
     st = got["stats"]
     assert st["fused"] == 1 and st["speculation_hit"] == 0 and st["probe_blocks"] == 0
-    want = _expected_groups(g, s, K, q, ref, st["tile_cols"])
+    by_mean = mode == "mean" or (mode == "paper" and ref["clique"]["success"])
+    T = MEAN_TILE if by_mean else st["tile_cols"]
+    want = _expected_groups(g, s, K, q, ref, T)
     assert st["repair_groups"] == want
     return got, ref, want
 
@@ -223,3 +228,25 @@ def test_repair_groups_of_two_tiles():
     T = got["stats"]["tile_cols"]
     assert T == 64 and _group_shift((d + T - 1) // T) == 1
     assert want == _groups_of(coords, T, d) == 3
+
+
+@pytest.mark.parametrize("mode", ["paper", "mean"])
+def test_repair_mean(mode):
+    """The weak attack with two adversaries (q < r: no file held by
+    adversaries alone) at four coordinates past the prefix: the prefix guess
+    (Case 1, every worker honest) and the final Case 1 (the honest workers)
+    keep every file and both take the mean, so its fp64 sums, in file order
+    either way, are redone only on the 1,024-coordinate tiles where a
+    moved file's replicas differ.  The mean kernel's grid (8 workgroups a
+    CU) takes two or three tiles a workgroup here."""
+    wl = synth.Workload(0, 7, 3, 2, 0, synth.DIST_NORMAL, "weak", "reversed", "fixed")
+    K, r, q = wl.K, wl.r, wl.q
+    d = MEAN_TILE * (2 * 8 * CUS + 5) + 12
+    s = oracle.assign(K, r)
+    coords = _coords(wl.f, d)
+    g = _attack_only_at(wl, s, d, coords)
+    print(f"mean repair: mode={mode} d={d}", flush=True)
+    got, ref, want = _repaired(g, K, r, q, mode=mode)
+    assert ref["clique"]["success"] and ref["n_selected"] == comb(K, r)
+    assert got["stats"]["tile_cols"] == 0   # the mean
+    assert want == len({c // MEAN_TILE for c in coords}) == 3
