@@ -456,7 +456,7 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": ("synthetic (seeded Philox, written on the GPU): "
                  + {synth.DIST_STUDENT3: "Student-t(3)", synth.DIST_TIED: "tied (1 + 16 random bits)"}
-                 .get(wl.dist, "Irwin-Hall N(0,0.01^2)")
+                 .get(wl.dist, "N(0,0.01^2) (polar method)")
                  + f" honest gradients, {wl.distortion} adversaries"),
         "config": {"workload": wl.name, "K": K, "r": r, "q": q, "files": f, "d": d,
                    **({"adversary_late": min(args.adversary_late, d)}

@@ -67,6 +67,11 @@ def _load():
     lib.synth_fill_device.restype = ctypes.c_int
     lib.synth_fnv1a.argtypes = [P, ctypes.c_int64]
     lib.synth_fnv1a.restype = ctypes.c_uint64
+    lib.synth_normal.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
+                                 ctypes.c_uint32, ctypes.c_uint64]
+    lib.synth_normal.restype = ctypes.c_double
+    lib.synth_log.argtypes = [ctypes.c_double]
+    lib.synth_log.restype = ctypes.c_double
     _lib = lib
     return lib
 
@@ -260,6 +265,16 @@ def generate(wl: Workload, subsets: np.ndarray, d: int | None = None, seed: int 
     role, worker, A, D = make_roles(wl, subsets, seed, **role_kw)
     g = fill(role, worker, 0, d, wl.dist, seed, wl.alie_z)
     return g, {"role": role, "worker": worker, "A": A, "D": D}
+
+
+def normal(seed: int, stream: int, sub: int, file: int, k: int) -> float:
+    """The generator's standard normal deviate of one counter."""
+    return float(_load().synth_normal(seed, stream, sub, file, k))
+
+
+def log(x: float) -> float:
+    """The generator's own natural logarithm (x > 0, normal)."""
+    return float(_load().synth_log(x))
 
 
 def fnv1a(buf: np.ndarray) -> int:

@@ -24,6 +24,10 @@ uint32_t synth_u32(uint64_t seed, uint32_t stream, uint64_t index);
 /* Honest gradient g_file[k] and a noise value for (worker, file, k). */
 float synth_honest_value(uint64_t seed, int32_t dist, uint32_t file, uint64_t k);
 float synth_noise_value(uint64_t seed, uint32_t worker, uint32_t file, uint64_t k);
+/* The standard normal deviate of a counter (polar method), and the natural
+ * logarithm of a positive normal double it uses (exposed for tests). */
+double synth_normal(uint64_t seed, uint32_t stream, uint32_t sub, uint32_t file, uint64_t k);
+double synth_log(double x);
 
 /* Fill out[f][r][nk] with coordinates [k0, k0+nk) of every replica.
  * role[i*r+s] picks the value of slot s of file i; worker[i*r+s] is the

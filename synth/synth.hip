@@ -14,8 +14,13 @@
  * numbers: as easy as 1, 2, 3", SC'11), counter-based, so any coordinate
  * range can be generated independently, in any order, on either side.
  *
- * Standard normal deviates: the Irwin-Hall construction Z = sum of 12
- * uniforms - 6 (unit variance, support [-6, 6]); its sum is exact in double.
+ * Standard normal deviates: the polar method (Marsaglia and Bray, "A
+ * convenient method for generating normal variables", SIAM Review 6, 1964):
+ * a point (v1, v2) uniform in the square [-1, 1)^2 from one Philox block,
+ * again from the next block while s = v1^2 + v2^2 is outside (0, 1), then
+ * Z = v1 * sqrt(-2 ln(s) / s).  The logarithm is computed here from the
+ * double's exponent and the series 2 atanh(t) of its mantissa (basic
+ * operations only, so both sides round alike).
  *
  * Values (the workload shapes of the paper's CIFAR-10 / ResNet-18 runs):
  *   honest   g_i[k] = fl32(0.01 * Z)                         (dist 0)
@@ -67,18 +72,46 @@ __host__ __device__ inline U4 philox(uint64_t seed, uint32_t c0, uint32_t c1, ui
     return U4{{c0, c1, c2, c3}};
 }
 
-// Irwin-Hall standard normal for counter (stream, sub, file, k):
-// 12 uniforms of 32 bits each from three Philox blocks.
+// Natural logarithm of a positive normal double, from x = m * 2^e with m in
+// [sqrt(1/2), sqrt(2)]: ln x = e ln 2 + 2 atanh(t), t = (m - 1) / (m + 1),
+// |t| <= 0.1716, the series to t^25 (the next term is below 1e-20 of it).
+__host__ __device__ inline double log_pos(double x) {
+    uint64_t b;
+    __builtin_memcpy(&b, &x, sizeof b);
+    int e = (int)((b >> 52) & 0x7FFu) - 1023;
+    b = (b & 0x000FFFFFFFFFFFFFull) | 0x3FF0000000000000ull;
+    double m;
+    __builtin_memcpy(&m, &b, sizeof m);
+    if (m > 1.4142135623730951) {
+        m *= 0.5;
+        ++e;
+    }
+    const double t = (m - 1.0) / (m + 1.0);
+    const double t2 = t * t;
+    double p = 1.0 / 25.0;
+    for (int j = 11; j >= 0; --j) p = p * t2 + 1.0 / (double)(2 * j + 1);
+    return (double)e * 0.69314718055994530942 + 2.0 * t * p;
+}
+
+// A double in [0, 1) from 53 random bits of two words (exact).
+__host__ __device__ inline double uniform53(uint32_t a, uint32_t b) {
+    return ((double)(a >> 5) * 67108864.0 + (double)(b >> 6)) * (1.0 / 9007199254740992.0);
+}
+
+// Standard normal for counter (stream, sub, file, k), by the polar method:
+// attempt a reads Philox block (k, file, 2^31 | stream << 16 | sub << 8 | a)
+// (attempts past 255, probability below 1e-170, give 0).
 __host__ __device__ inline double normal(uint64_t seed, uint32_t stream, uint32_t sub,
                                          uint32_t file, uint64_t k) {
-    uint64_t s = 0;
-    for (uint32_t b = 0; b < 3; ++b) {
+    for (uint32_t a = 0; a < 256u; ++a) {
         const U4 u = philox(seed, (uint32_t)k, (uint32_t)(k >> 32), file,
-                            (stream << 8) | (sub << 2) | b);
-        s += (uint64_t)u.x[0] + u.x[1] + u.x[2] + u.x[3];
+                            0x80000000u | (stream << 16) | (sub << 8) | a);
+        const double v1 = 2.0 * uniform53(u.x[0], u.x[1]) - 1.0;
+        const double v2 = 2.0 * uniform53(u.x[2], u.x[3]) - 1.0;
+        const double s = v1 * v1 + v2 * v2;
+        if (s > 0.0 && s < 1.0) return v1 * sqrt(-2.0 * log_pos(s) / s);
     }
-    const int64_t centred = (int64_t)s - (int64_t)6 * 4294967296ll;   // exact
-    return (double)centred * (1.0 / 4294967296.0);                      // exact
+    return 0.0;
 }
 
 __host__ __device__ inline float honest_value(uint64_t seed, int32_t dist, uint32_t file,
@@ -246,6 +279,12 @@ float synth_honest_value(uint64_t seed, int32_t dist, uint32_t file, uint64_t k)
 float synth_noise_value(uint64_t seed, uint32_t worker, uint32_t file, uint64_t k) {
     return noise_value(seed, worker, file, k);
 }
+
+double synth_normal(uint64_t seed, uint32_t stream, uint32_t sub, uint32_t file, uint64_t k) {
+    return normal(seed, stream, sub, file, k);
+}
+
+double synth_log(double x) { return log_pos(x); }
 
 int synth_fill(const uint8_t *role, const int32_t *worker, int64_t f, int32_t r, int64_t k0,
                int64_t nk, int32_t dist, uint64_t seed, double alie_z, float *out,

@@ -40,3 +40,46 @@ def test_adversary_choice_is_seeded():
     a1 = synth.choose_adversaries(wl, s, 428)
     assert a1 == synth.choose_adversaries(wl, s, 428)
     assert len(a1) == wl.q and len(set(a1)) == wl.q
+
+
+def test_log_matches_libm():
+    """The generator's own logarithm (basic operations only, so host and
+    device round alike) against the C library's, over the range the polar
+    method feeds it (0, 1) and beyond."""
+    import math
+    rng = np.random.default_rng(7)
+    xs = np.concatenate([rng.random(20000), 10.0 ** rng.uniform(-300, 300, 20000),
+                         [2.0 ** -1022, 2.0 ** -106, 0.5, 1.0 - 2.0 ** -53, 1.0,
+                          math.sqrt(0.5), math.sqrt(2.0), 1.4142135623730951]])
+    worst = 0.0   # in units in the last place of the C library's result
+    for x in xs:
+        x = float(x)
+        ref = math.log(x)
+        if ref != 0.0:
+            worst = max(worst, abs(synth.log(x) - ref) / math.ulp(ref))
+    assert synth.log(1.0) == 0.0
+    assert worst <= 2.0, worst
+
+
+def test_normal_deviates_are_standard_normal():
+    """The polar method's deviates: mean 0, variance 1, third and fourth
+    moments 0 and 3, tails past the +-6 that a sum of 12 uniforms cannot
+    reach, and the normal CDF at several points (Kolmogorov-Smirnov against
+    the exact CDF).  Counters are independent across k, file and stream."""
+    import math
+    from scipy import stats
+    n = 200_000
+    z = np.array([synth.normal(synth.SEED, 1, 0, f, k) for f in range(2) for k in range(n // 2)])
+    assert abs(z.mean()) < 0.01
+    assert abs(z.var() - 1.0) < 0.015
+    assert abs(stats.skew(z)) < 0.03
+    assert abs(stats.kurtosis(z, fisher=False) - 3.0) < 0.06
+    assert stats.kstest(z, "norm").pvalue > 1e-3
+    # the tail: P(|Z| > 4) = 6.3e-5, so about 13 of 200,000
+    assert 3 <= int((np.abs(z) > 4.0).sum()) <= 30
+    far = max(abs(synth.normal(synth.SEED, 1, 0, 7, k)) for k in range(2_000_000, 2_400_000))
+    assert far > 4.5
+    # another stream or file gives another sequence
+    other = np.array([synth.normal(synth.SEED, 2, 0, 0, k) for k in range(1000)])
+    assert abs(np.corrcoef(z[:1000], other)[0, 1]) < 0.15
+    assert math.isfinite(float(np.abs(z).max()))
