@@ -28,9 +28,10 @@
  * the stream (it needs the agreement graph on the host) and returns with
  * its work complete.
  *
- * Thread safety: re-entrant.  Global state: the per-thread error message
- * and a per-device cache of the compute-unit count (written once per device
- * with relaxed atomics).  Calls that share output buffers must not overlap.
+ * Thread safety: re-entrant.  Global state: the per-thread error message,
+ * a per-device cache of the compute-unit count (written once per device
+ * with relaxed atomics) and the probe's random base (drawn once) and call
+ * counter (an atomic).  Calls that share output buffers must not overlap.
  */
 #ifndef ASPIS_H
 #define ASPIS_H

@@ -293,9 +293,14 @@ int64_t probe_coords(int64_t f, int64_t d) {
 // The seed of a probe drawn for this call: SplitMix64 of a per-process
 // random base and a call counter (never 0, which denotes the prefix).
 uint64_t probe_seed() {
-    static const uint64_t base = [] {
-        std::random_device rd;
-        return ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+    static const uint64_t base = []() -> uint64_t {
+        // the system's entropy source; the clock if it cannot be opened
+        try {
+            std::random_device rd;
+            return ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+        } catch (...) {
+            return (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+        }
     }();
     static std::atomic<uint64_t> calls{0};
     const uint64_t x = aspis::splitmix64(base + calls.fetch_add(1, std::memory_order_relaxed));
