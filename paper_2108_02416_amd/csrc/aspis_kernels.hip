@@ -65,14 +65,30 @@ __device__ __forceinline__ uint32_t from_key(uint32_t k) {
 // Offsets below 16 use DPP row permutations: after the two quad steps every
 // lane of a quad holds the quad's value, and the half-row / row mirrors pair
 // each lane with one lane of the other half.
-enum class Op { And, Or, Add, Max };
+enum class Op { And, Or, Add, Max, Min };
 
 template <Op OP>
 __device__ __forceinline__ uint32_t combine(uint32_t a, uint32_t b) {
     if constexpr (OP == Op::And) return a & b;
     if constexpr (OP == Op::Or) return a | b;
     if constexpr (OP == Op::Max) return a > b ? a : b;
+    if constexpr (OP == Op::Min) return a < b ? a : b;
     return a + b;
+}
+
+// Two 16-bit unsigned lanes of a word at once (v_pk_min_u16, v_pk_max_u16,
+// v_pk_add_u16: integer lanes, no carry between them).
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_min(__builtin_bit_cast(u16x2, a),
+                                                                  __builtin_bit_cast(u16x2, b)));
+}
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2, a),
+                                                                  __builtin_bit_cast(u16x2, b)));
+}
+__device__ __forceinline__ uint32_t pk_add_u16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, a) + __builtin_bit_cast(u16x2, b));
 }
 
 template <int CTRL>
@@ -421,12 +437,14 @@ __device__ __forceinline__ void put_pairs(uint32_t *tile, int p, int cq, const u
 // row.  hist: half_hist_words(T) words, zero on entry and on exit.  The
 // tile is overwritten.
 //
-//  1. one pass: the common magnitude bits of the keys below 0xFFFF, the
-//     count of sign-clear keys and of 0xFFFF keys; settles the sign (or
-//     H = 0xFFFF when the rank falls among those);
-//  2. histogram rounds over the 16-bit keys, each resolving kHalfWindow bits
-//     below the last settled one, until the sought high half H is known
-//     (at most 3 rounds); nothing is compacted, every round reads all keys;
+//  1. one pass: the least key, the greatest key below 0xFFFF, the least
+//     sign-set and the greatest sign-clear key, and the count of sign-set
+//     keys (packed 16-bit min / max / add, two keys an instruction); settles
+//     the sign and the window [lo, hi] of the keys of that sign;
+//  2. histogram rounds over the window, each resolving kHalfWindow bits,
+//     until the sought high half H is known (at most 3 rounds; H = 0xFFFF
+//     when the rank falls past a sign-set window); nothing is compacted,
+//     every round reads all keys;
 //  3. one pass collecting the rows whose high half is H into the lane's
 //     16-bit slots (in place), then their low halves are read from g;
 //  4. bitwise radix select on those low halves for the remaining rank.
@@ -469,19 +487,19 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         return base16[(x >> 1) * 2 * STRIDE + (x & 1)];
     };
 
-    // 1. common magnitude bits (keys below 0xFFFF), sign-set and 0xFFFF
-    //    counts, both keys of a word at once in 16-bit lanes (no carry or
-    //    borrow crosses the halves; counts stay below 2^16)
-    uint32_t am2 = 0x7FFF7FFFu, om2 = 0u, zs2 = 0u, nn2 = 0u;
+    // 1. extremes and the sign count, both keys of a word at once in 16-bit
+    //    lanes: the least key, the greatest key below 0xFFFF (the greatest
+    //    key + 1, which wraps 0xFFFF to 0), and with the sign bit flipped the
+    //    least sign-set key and the greatest sign-clear key; the number of
+    //    sign-set keys
+    uint32_t mn2 = 0xFFFFFFFFu, mt2 = 0u, ms2 = 0xFFFFFFFFu, mc2 = 0u, ns = 0u;
     auto stats = [&](uint32_t w) __attribute__((always_inline)) {
-        const uint32_t s2 = w & 0x80008000u;                         // sign-set keys
-        const uint32_t mag2 = (w ^ (0x7FFF7FFFu ^ (s2 - (s2 >> 15)))) & 0x7FFF7FFFu;
-        const uint32_t nt = ~w;                                      // zero: key 0xFFFF
-        const uint32_t nz2 = (((nt & 0x7FFF7FFFu) + 0x7FFF7FFFu) | nt) & 0x80008000u;
-        am2 &= mag2;
-        om2 |= mag2 & (nz2 - (nz2 >> 15));
-        zs2 += s2 >> 15;
-        nn2 += nz2 >> 15;
+        const uint32_t x = w ^ 0x80008000u;
+        mn2 = pk_min_u16(mn2, w);
+        mt2 = pk_max_u16(mt2, pk_add_u16(w, 0x00010001u));
+        ms2 = pk_min_u16(ms2, x);
+        mc2 = pk_max_u16(mc2, x);
+        ns += (uint32_t)__builtin_popcount(w & 0x80008000u);
     };
     {
         int x = 0;
@@ -494,78 +512,79 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         }
         for (; x < cnt; ++x) stats(base[x * STRIDE]);
     }
-    uint32_t am = group_reduce<G, Op::And>(am2 & (am2 >> 16) & 0x7FFFu);
-    uint32_t om = group_reduce<G, Op::Or>((om2 | (om2 >> 16)) & 0x7FFFu);
-    const uint32_t z = (uint32_t)(2 * np) -
-                       group_reduce<G, Op::Add>((zs2 & 0xFFFFu) + (zs2 >> 16));   // sign-clear
-    const uint32_t top = (uint32_t)(2 * np) -
-                         group_reduce<G, Op::Add>((nn2 & 0xFFFFu) + (nn2 >> 16));
+    auto lo16 = [](uint32_t v2, bool lower) __attribute__((always_inline)) {
+        const uint32_t a = v2 & 0xFFFFu, b = v2 >> 16;
+        return lower ? (a < b ? a : b) : (a > b ? a : b);
+    };
+    const uint32_t mn = group_reduce<G, Op::Min>(lo16(mn2, true));                // least key
+    const uint32_t mt = group_reduce<G, Op::Max>(lo16(mt2, false));               // greatest below 0xFFFF, + 1
+    const uint32_t ms = group_reduce<G, Op::Min>(lo16(ms2, true)) ^ 0x8000u;      // least sign-set
+    const uint32_t mc = group_reduce<G, Op::Max>(lo16(mc2, false)) ^ 0x8000u;     // greatest sign-clear
+    const uint32_t z = (uint32_t)(2 * np) - group_reduce<G, Op::Add>(ns);         // sign-clear count
 
-    uint32_t H;
-    uint32_t sgn = 0x8000u;
+    // 2. the window [lo, hi] of the keys of the sought key's sign (below
+    //    0xFFFF); histogram rounds split it into kHalfBuckets buckets of
+    //    2^sh keys and keep the one holding rank m, until sh = 0 (16 bits:
+    //    three rounds at most).  A key above hi inside the window (0xFFFF, or
+    //    a sign-set key in a sign-clear window) is counted like any other:
+    //    it is above the sought key.  The rank past a sign-set window is a
+    //    0xFFFF key.
+    uint32_t H = kHalfTop;
     bool settled = false;
+    uint32_t lo, hi;
     if (m < z) {
-        sgn = 0u;
+        lo = mn;
+        hi = mc;
     } else {
         m -= z;
-        const uint32_t below_top = (uint32_t)(2 * np) - z - top;   // sign-set keys below 0xFFFF
-        if (m >= below_top) {
-            H = kHalfTop;
-            m -= below_top;
-            settled = true;
-        }
+        lo = ms;
+        hi = mt - 1u;
+        if (mt == 0u || hi < lo) settled = true;   // no sign-set key below 0xFFFF
     }
     if (!settled) {
-        const uint32_t vm = am ^ om;
-        if (vm == 0u) {   // one magnitude: the sign gives the key
-            H = sgn ? (0x8000u | am) : (~am & 0x7FFFu);
-        } else {
-            // 2. the keys of the sign below 0xFFFF lie in [bias, bias +
-            //    2^(hb+1)); each round splits the window into buckets of 2^sh
-            //    keys and keeps the one holding rank m (a 0xFFFF key inside
-            //    the window is counted like any other; one above it is above
-            //    the sought rank)
-            int hb = 31 - __clz(vm);
-            const uint32_t hi = 0x7FFFu & ~((2u << hb) - 1u);
-            uint32_t bias = sgn ? (0x8000u | (am & hi)) : (~am & hi);
-            for (int round = 0; round < 3; ++round) {
-                const int sh = hb >= kHalfWindow - 1 ? hb - (kHalfWindow - 1) : 0;
-                const uint32_t span = 2u << hb;
-                each([&](uint32_t k, int, int) {
-                    const uint32_t o = k - bias;
-                    if (o < span) atomicAdd(&hcol[o >> sh], 1u);
-                });
-                uint32_t h[BPL];
+        uint32_t bias = lo;
+        const int width = 32 - __clz(hi - lo);   // bits of hi - lo (0 when equal)
+        int sh = width > kHalfWindow ? width - kHalfWindow : 0;
+        for (int round = 0; round < 3; ++round) {
+            const uint32_t span = (uint32_t)kHalfBuckets << sh;
+            each([&](uint32_t k, int, int) {
+                const uint32_t o = k - bias;
+                if (o < span) atomicAdd(&hcol[o >> sh], 1u);
+            });
+            uint32_t h[BPL];
 #pragma unroll
-                for (int q = 0; q < BPL; q += 2) {
-                    const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[gl * BPL + q]);
-                    h[q] = w2.x;
-                    h[q + 1] = w2.y;
-                }
-#pragma unroll
-                for (int q = 0; q < BPL; q += 2)
-                    *reinterpret_cast<uint2 *>(&hcol[gl * BPL + q]) = make_uint2(0u, 0u);
-                uint32_t tot = 0u;
-#pragma unroll
-                for (int q = 0; q < BPL; ++q) tot += h[q];
-                uint32_t run = group_scan<G>(tot, gl) - tot;
-                uint32_t le = 0u, below = 0u;
-#pragma unroll
-                for (int q = 0; q < BPL; ++q) {
-                    run += h[q];
-                    const bool ok = run <= m;
-                    le += ok ? 1u : 0u;
-                    below = ok ? run : below;
-                }
-                le = group_reduce<G, Op::Add>(le);
-                below = group_reduce<G, Op::Max>(below);
-                m -= below;
-                bias += le << sh;
-                if (sh == 0) break;   // 15 bits: windows 14..9, 8..3, 2..0 at most
-                hb = sh - 1;
+            for (int q = 0; q < BPL; q += 2) {
+                const uint2 w2 = *reinterpret_cast<const uint2 *>(&hcol[gl * BPL + q]);
+                h[q] = w2.x;
+                h[q + 1] = w2.y;
             }
-            H = bias;
+#pragma unroll
+            for (int q = 0; q < BPL; q += 2)
+                *reinterpret_cast<uint2 *>(&hcol[gl * BPL + q]) = make_uint2(0u, 0u);
+            uint32_t tot = 0u;
+#pragma unroll
+            for (int q = 0; q < BPL; ++q) tot += h[q];
+            uint32_t run = group_scan<G>(tot, gl) - tot;
+            uint32_t le = 0u, below = 0u;
+#pragma unroll
+            for (int q = 0; q < BPL; ++q) {
+                run += h[q];
+                const bool ok = run <= m;
+                le += ok ? 1u : 0u;
+                below = ok ? run : below;
+            }
+            le = group_reduce<G, Op::Add>(le);
+            below = group_reduce<G, Op::Max>(below);
+            m -= below;
+            if (le == (uint32_t)kHalfBuckets) {   // past the window: a 0xFFFF key
+                settled = true;
+                break;
+            }
+            bias += le << sh;
+            if (sh == 0) break;
+            sh = sh > kHalfWindow ? sh - kHalfWindow : 0;
         }
+        if (!settled) H = bias;
     }
 
     // 3. rows whose high half is H, as row numbers in the lane's slots (the
