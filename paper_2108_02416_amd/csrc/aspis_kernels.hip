@@ -529,10 +529,19 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     //    a sign-set key in a sign-clear window) is counted like any other:
     //    it is above the sought key.  The rank past a sign-set window is a
     //    0xFFFF key.
+    //    The round of single keys (sh = 0) also lists the lane's keys in its
+    //    window as (word, half, bucket) codes in the lane's 16-bit slots, in
+    //    place (the write cursor never passes the read cursor), and keeps
+    //    those of the sought bucket as row numbers: step 3 then has its rows
+    //    without another pass.  Not in a first round that may find the rank
+    //    past a sign-set window (the tile must stay whole for the 0xFFFF
+    //    pass), nor when a lane holds 512 words or more (9 bits of word).
     uint32_t H = kHalfTop;
-    bool settled = false;
+    bool settled = false, collected = false;
+    int w = 0;
     uint32_t lo, hi;
-    if (m < z) {
+    const bool clear_sign = m < z;
+    if (clear_sign) {
         lo = mn;
         hi = mc;
     } else {
@@ -547,10 +556,22 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         int sh = width > kHalfWindow ? width - kHalfWindow : 0;
         for (int round = 0; round < 3; ++round) {
             const uint32_t span = (uint32_t)kHalfBuckets << sh;
-            each([&](uint32_t k, int, int) {
-                const uint32_t o = k - bias;
-                if (o < span) atomicAdd(&hcol[o >> sh], 1u);
-            });
+            const bool list = sh == 0 && (round > 0 || clear_sign) && np <= 511 * G;
+            if (list) {
+                each([&](uint32_t k, int x, int hf) {
+                    const uint32_t o = k - bias;
+                    if (o < span) {
+                        atomicAdd(&hcol[o], 1u);
+                        slot(w) = (uint16_t)(((uint32_t)x << 7) | ((uint32_t)hf << 6) | o);
+                        ++w;
+                    }
+                });
+            } else {
+                each([&](uint32_t k, int, int) {
+                    const uint32_t o = k - bias;
+                    if (o < span) atomicAdd(&hcol[o >> sh], 1u);
+                });
+            }
             uint32_t h[BPL];
 #pragma unroll
             for (int q = 0; q < BPL; q += 2) {
@@ -581,7 +602,21 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
                 break;
             }
             bias += le << sh;
-            if (sh == 0) break;
+            if (sh == 0) {
+                if (list) {   // the listed keys of bucket le, as row numbers
+                    int n2 = 0;
+                    for (int j = 0; j < w; ++j) {
+                        const uint32_t v = slot(j);
+                        if ((v & 63u) == le) {
+                            slot(n2) = (uint16_t)half_row<RPI>(gl + (int)(v >> 7) * G, (int)(v >> 6) & 1);
+                            ++n2;
+                        }
+                    }
+                    w = n2;
+                    collected = true;
+                }
+                break;
+            }
             sh = sh > kHalfWindow ? sh - kHalfWindow : 0;
         }
         if (!settled) H = bias;
@@ -589,13 +624,15 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
 
     // 3. rows whose high half is H, as row numbers in the lane's slots (the
     //    write cursor never passes the read cursor), then their low halves
-    int w = 0;
-    each([&](uint32_t k, int x, int h) {
-        if (k == H) {
-            slot(w) = (uint16_t)half_row<RPI>(gl + x * G, h);
-            ++w;
-        }
-    });
+    if (!collected) {
+        w = 0;
+        each([&](uint32_t k, int x, int hf) {
+            if (k == H) {
+                slot(w) = (uint16_t)half_row<RPI>(gl + x * G, hf);
+                ++w;
+            }
+        });
+    }
     const bool valid = k0 + c < d;
     constexpr int kGather = 4;   // row reads in flight per lane
     for (int x0 = 0; x0 < w; x0 += kGather) {
