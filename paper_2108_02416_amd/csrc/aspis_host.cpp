@@ -456,11 +456,13 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
         decide_keys(rows);
         return aspis_clique(rows, K, q, out_res);
     };
-    // the row of every replica in a worker-major upload, in the workspace.
-    // The host copy must outlive the asynchronous upload: the guard, declared
-    // after it and so destroyed before it, waits for the stream on every
-    // return (a no-op after the synchronisations of a normal return)
+    // the row of every replica in a worker-major upload, in the workspace,
+    // and the repair's group count copied back.  The host memory must
+    // outlive the asynchronous copies: the guard, declared after it and so
+    // destroyed before it, waits for the stream on every return once armed
+    // (a no-op after the synchronisations of a normal return)
     std::vector<int32_t> host_rows;
+    int32_t groups = -1;
     struct DrainStream {
         hipStream_t s;
         bool armed = false;
@@ -554,7 +556,6 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                 ASPIS_HIP(aspis::launch_select(subsets_dev, det->vote, f, r, res->success,
                                                honest_mask(res), row_of, ws, sel_out, nullptr, 0,
                                                s));
-            int32_t groups = -1;
             if (!hit) {
                 fused_tile = aspis::TileUse{};
                 if (repair) {
@@ -566,6 +567,7 @@ aspis_status detect_aggregate_impl(const float *grads, bool worker_major, int32_
                     else
                         ASPIS_HIP(aspis::launch_median(grads, d, ws, f, out, s, &fused_tile,
                                                        full_keys, true));
+                    drain.armed = true;
                     ASPIS_HIP(hipMemcpyAsync(&groups, ws.repair, sizeof(int32_t),
                                              hipMemcpyDeviceToHost, s));
                 } else if (final_mean) {
