@@ -250,3 +250,23 @@ def test_repair_mean(mode):
     assert ref["clique"]["success"] and ref["n_selected"] == comb(K, r)
     assert got["stats"]["tile_cols"] == 0   # the mean
     assert want == len({c // MEAN_TILE for c in coords}) == 3
+
+
+@pytest.mark.parametrize("extra", [4, 5, 1029])
+def test_drawn_probe_just_past_its_length(extra):
+    """A vector a few coordinates longer than the probe (32,768 coordinates at
+    455 files): the 32 blocks are drawn from the few positions there are
+    (also with d odd, the scalar-load paths), and the result is the oracle's,
+    with every worker honest and with the attack everywhere."""
+    wl = synth.WORKLOADS[3]
+    K, r, q = wl.K, wl.r, wl.q
+    d = 32768 + extra
+    s = oracle.assign(K, r)
+    g, _ = synth.generate(wl, s, d=d)
+    for data in (g, _attack_only_at(wl, s, d, [])):
+        ref = _oracle(data, K, r, q, "median")
+        got = _run(data, K, r, q)
+        _compare(got, ref, K, "median")
+        st = got["stats"]
+        assert st["probe_blocks"] == 32 and st["probe_coords"] == 32768 and st["fused"] == 1
+        assert st["speculation_hit"] == 1
