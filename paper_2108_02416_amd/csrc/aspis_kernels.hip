@@ -435,7 +435,11 @@ __device__ __forceinline__ void put_pairs(uint32_t *tile, int p, int cq, const u
 // stid = c*G + g of column c, written to out[k0 + c] for k0 + c < d.
 // row(j) gives the replica row of g behind tile row j, or -1 for a padding
 // row.  hist: half_hist_words(T) words, zero on entry and on exit.  The
-// tile is overwritten.
+// tile is overwritten.  With REG > 0 (np a multiple of G, np / G <= REG)
+// the lane's words are read from the tile once, into registers, and every
+// later pass over the keys reads those (the median kernel measured 4-5 %
+// faster at 455 rows; the single pass, whose registers are taken by its
+// own state, keeps reading the tile).
 //
 //  1. one pass: the least key, the greatest key below 0xFFFF, the least
 //     sign-set and the greatest sign-clear key, and the count of sign-set
@@ -448,7 +452,7 @@ __device__ __forceinline__ void put_pairs(uint32_t *tile, int p, int cq, const u
 //  3. one pass collecting the rows whose high half is H into the lane's
 //     16-bit slots (in place), then their low halves are read from g;
 //  4. bitwise radix select on those low halves for the remaining rank.
-template <int T, int G, int RPI, typename RowFn>
+template <int T, int G, int RPI, int REG = 0, typename RowFn>
 __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist, int np, int nk,
                                                  int64_t k0, int64_t d, float *out, int stid,
                                                  const float *__restrict__ g, RowFn &&row) {
@@ -462,9 +466,27 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     uint32_t *hcol = hist + c * kHalfStride;
     const int cnt = np > gl ? (np - gl + G - 1) / G : 0;   // words of this lane
     uint32_t m = (uint32_t)(nk - 1) / 2;
+    // REG > 0: the lane's words (np a multiple of G: the same count in every
+    // lane, at most REG) are read once, into registers
+    uint32_t kw[REG > 0 ? REG : 1];
+    const int cw = __builtin_amdgcn_readfirstlane(cnt);
 
     // every key of the lane: fn(key, word x, half h) for pair-row gl + x*G
     auto each = [&](auto &&fn) __attribute__((always_inline)) {
+        if constexpr (REG > 0) {
+            // cw is a multiple of 4 (np is a multiple of RPI = 4G)
+#pragma unroll
+            for (int xb = 0; xb < REG; xb += 4) {
+                if (xb < cw) {
+#pragma unroll
+                    for (int x = xb; x < xb + 4 && x < REG; ++x) {
+                        fn(kw[x] & 0xFFFFu, x, 0);
+                        fn(kw[x] >> 16, x, 1);
+                    }
+                }
+            }
+            return;
+        }
         int x = 0;
         for (; x + kSelBatch <= cnt; x += kSelBatch) {
             uint32_t v[kSelBatch];
@@ -501,7 +523,22 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
         mc2 = pk_max_u16(mc2, x);
         ns += (uint32_t)__builtin_popcount(w & 0x80008000u);
     };
-    {
+    if constexpr (REG > 0) {
+#pragma unroll
+        for (int xb = 0; xb < REG; xb += 4) {
+            if (xb < cw) {
+#pragma unroll
+                for (int x = xb; x < xb + 4 && x < REG; ++x) kw[x] = base[x * STRIDE];
+            }
+        }
+#pragma unroll
+        for (int xb = 0; xb < REG; xb += 4) {
+            if (xb < cw) {
+#pragma unroll
+                for (int x = xb; x < xb + 4 && x < REG; ++x) stats(kw[x]);
+            }
+        }
+    } else {
         int x = 0;
         for (; x + kSelBatch <= cnt; x += kSelBatch) {
             uint32_t v[kSelBatch];
@@ -1561,8 +1598,11 @@ median_ws_kernel(const float *__restrict__ g, int64_t d, const int32_t *__restri
                 auto row = [&](int j) __attribute__((always_inline)) -> int64_t {
                     return j < n ? (int64_t)rl[j] : -1;
                 };
-                select_half_tile<T, G, RPI>(tile, hist, (int)half_pair_rows(n, T, FILL), n, t * T, d,
-                                            out, tid - FILL, g, row);
+                // FILL = 512: RPI = 4G, so every lane holds the same number of
+                // words, at most 2 SW
+                constexpr int REG = (FILL == kWsFill && RPI == 4 * G) ? 2 * SW : 0;
+                select_half_tile<T, G, RPI, REG>(tile, hist, (int)half_pair_rows(n, T, FILL), n,
+                                                 t * T, d, out, tid - FILL, g, row);
             } else {
                 select_tile<T, G>(tile, hist, n, t * T, d, out, tid - FILL);
             }
