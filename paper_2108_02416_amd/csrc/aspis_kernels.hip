@@ -466,8 +466,10 @@ __device__ __forceinline__ void select_half_tile(uint32_t *tile, uint32_t *hist,
     uint32_t *hcol = hist + c * kHalfStride;
     const int cnt = np > gl ? (np - gl + G - 1) / G : 0;   // words of this lane
     uint32_t m = (uint32_t)(nk - 1) / 2;
-    // REG > 0: the lane's words (np a multiple of G: the same count in every
-    // lane, at most REG) are read once, into registers
+    // REG > 0: the lane's words are read once, into registers.  The caller
+    // passes np = half_pair_rows(...), a multiple of RPI = 4G, so every lane
+    // of the wave holds the same count, a multiple of 4, at most REG
+    static_assert(REG == 0 || RPI == 4 * G, "register mode needs RPI = 4G");
     uint32_t kw[REG > 0 ? REG : 1];
     const int cw = __builtin_amdgcn_readfirstlane(cnt);
 
