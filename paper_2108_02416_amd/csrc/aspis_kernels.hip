@@ -139,7 +139,7 @@ constexpr int tile_block() { return T >= 16 ? 1024 : 64 * T; }
 // G lanes of a column read rows j == g (mod G); the swizzle puts the 32
 // lanes of every half-wave in 32 distinct banks.
 template <int T, int G>
-__device__ __forceinline__ int tile_swz(int g) {
+__host__ __device__ constexpr int tile_swz_of(int g) {
     static_assert(T == 4 || T == 8 || T == 16 || T == 32 || T == 64 || T == 128, "tile width");
     static_assert(G >= 1 && G <= 64 && (G & (G - 1)) == 0, "lanes per column");
     if constexpr (T >= 32) {
@@ -148,6 +148,30 @@ __device__ __forceinline__ int tile_swz(int g) {
     } else {
         return (g / (32 / T)) & (T - 1);
     }
+}
+
+// The promise above, checked at compile time for every (T, G) the kernels
+// instantiate: the first word each lane of a half-wave reads lies in a bank
+// (of 32) of its own.  A lane's later rows lie G*T words further, a multiple
+// of 32, so they keep the same banks.
+template <int T, int G>
+constexpr bool tile_swz_conflict_free() {
+    for (int h = 0; h < T * G; h += 32) {
+        uint32_t used = 0;
+        for (int i = h; i < h + 32 && i < T * G; ++i) {
+            const int c = i / G, g = i % G;
+            const int bank = (g * T + (c ^ tile_swz_of<T, G>(g))) % 32;
+            if (used & (1u << bank)) return false;
+            used |= 1u << bank;
+        }
+    }
+    return true;
+}
+
+template <int T, int G>
+__device__ __forceinline__ int tile_swz(int g) {
+    static_assert(tile_swz_conflict_free<T, G>(), "tile swizzle leaves a bank conflict");
+    return tile_swz_of<T, G>(g);
 }
 
 // Store the keys of row j, columns 4cq..4cq+3.
