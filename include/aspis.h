@@ -15,8 +15,10 @@
  * where slot s of file i is the s-th smallest worker of the file's subset.
  *
  * Ownership: every buffer is allocated and freed by the caller.  The library
- * keeps no device memory between calls; what it needs beyond inputs and
- * outputs comes through the caller's workspace.
+ * allocates no device memory: what it needs beyond inputs and outputs comes
+ * through the caller's workspace, or, for aspis_detect_aggregate_noalloc,
+ * from a static device array (ASPIS_NOALLOC_SCRATCH_BYTES per device) that
+ * is part of the loaded library.
  *
  * Errors: every entry point returns an aspis_status and never throws.  On
  * ASPIS_ERR_INVALID_ARG / ASPIS_ERR_OVERFLOW nothing has been written or
@@ -30,8 +32,10 @@
  *
  * Thread safety: re-entrant.  Global state: the per-thread error message,
  * a per-device cache of the compute-unit count (written once per device
- * with relaxed atomics) and the probe's random base (drawn once) and call
- * counter (an atomic).  Calls that share output buffers must not overlap.
+ * with relaxed atomics), the probe's random base (drawn once) and call
+ * counter (an atomic), and the allocation-free entry point's static scratch
+ * array with its per-device address.  Calls that share output buffers, and
+ * allocation-free calls on one device, must not overlap.
  */
 #ifndef ASPIS_H
 #define ASPIS_H
