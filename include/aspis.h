@@ -174,7 +174,7 @@ typedef struct {
     int64_t probe_coords;      /* coordinates the guess was taken from      */
     float ms_probe;            /* agreement pass over the probe             */
     float ms_main;             /* main pass (fused, or detect + reduce)     */
-    float ms_fallback;         /* reduction rerun after a wrong guess       */
+    float ms_fallback;         /* repair or rerun after a wrong guess       */
     float ms_total;            /* first kernel to result, host steps incl.  */
     int32_t tile_cols;         /* coordinates per tile of the median kernel
                                   that produced out (0: the mean)          */
@@ -187,10 +187,10 @@ typedef struct {
     int32_t probe_blocks;      /* blocks of 1,024 coordinates at positions
                                   drawn per call; 0: the probe was the
                                   prefix                                   */
-    int32_t repair_groups;     /* after a wrong guess that kept the same
-                                  files for the same median: the tile groups
+    int32_t repair_groups;     /* after a wrong guess that asked for the
+                                  same reduction: the tile groups
                                   recomputed (the others kept the guessed
-                                  median, already final there); -1 if the
+                                  result, already final there); -1 if the
                                   step did not repair                      */
 } aspis_run_stats;
 
@@ -214,13 +214,14 @@ typedef struct {
  * 1,024 coordinates at positions drawn per call (SplitMix64 of a random
  * per-process seed and a call counter), so that a worker cannot know when
  * it uploads which coordinates the guess reads; ASPIS_FLAG_PROBE_PREFIX
- * takes the prefix instead.  After a wrong guess that kept the same files
- * and asked for the same median, only the tiles holding a coordinate where
- * some file's guessed and final replicas differ are recomputed.
+ * takes the prefix instead.  After a wrong guess that asked for the same
+ * reduction as the final detection, only the tiles holding a coordinate
+ * where some file's guessed and final replicas differ are recomputed
+ * (every tile when the guess kept other files).
  * Median tiles: the half-key tiles keep only the high 16 bits of each key
  * in LDS (twice the columns) and read back the low halves of the rows tied
  * with the median's high half.  Unless a key flag says otherwise, a tie
- * probe over the prefix decides: when at a typical probed coordinate 64 or
+ * probe over 64 of the probed coordinates decides: when at a typical probed coordinate 64 or
  * more files share the median's high half, the step takes full-key tiles
  * (no read-back).  The choice changes the speed, never the result.
  *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
