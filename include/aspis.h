@@ -181,9 +181,10 @@ typedef struct {
     int32_t half_keys;         /* 1 if that tile held only the high 16 bits
                                   of each key (low halves read back)       */
     int32_t tie_rows;          /* tie probe: over the probed coordinates,
-                                  the median of the number of files whose
-                                  value shares the high 16-bit key half of
-                                  the files' median; -1 if not probed     */
+                                  the mean (rounded up) of the number of
+                                  files whose value shares the high 16-bit
+                                  key half of the files' median; -1 if not
+                                  probed                                   */
     int32_t probe_blocks;      /* blocks of 1,024 coordinates at positions
                                   drawn per call; 0: the probe was the
                                   prefix                                   */
@@ -221,9 +222,9 @@ typedef struct {
  * Median tiles: the half-key tiles keep only the high 16 bits of each key
  * in LDS (twice the columns) and read back the low halves of the rows tied
  * with the median's high half.  Unless a key flag says otherwise, a tie
- * probe over 64 of the probed coordinates decides: when at a typical probed coordinate 64 or
- * more files share the median's high half, the step takes full-key tiles
- * (no read-back).  The choice changes the speed, never the result.
+ * probe over 64 of the probed coordinates decides: when on average 16 or
+ * more files there share the median's high half, the step takes full-key
+ * tiles (no read-back).  The choice changes the speed, never the result.
  *   det, res, out, sel_out, n_selected  as above (sel_out may be NULL)
  *   flags   ASPIS_FLAG_* ; stats may be NULL.
  * Errors as aspis_aggregate's, except that on NO_FILES `out` holds no

@@ -162,25 +162,24 @@ bool use_mean(aspis_reduce mode, const aspis_clique_result *res) {
     return mode == ASPIS_REDUCE_MEAN || (mode == ASPIS_REDUCE_PAPER && res->success);
 }
 
-// Full-key tiles when at a typical probed coordinate at least this many
-// files share the high 16-bit key half of the median.  Below it the
-// half-key tiles' read-back stays small: 28 files tied with the median
-// (ALIE colluders sending the honest mean, K = 15) cost the half-key single
-// pass as much as the full-key one.
-constexpr uint32_t kTieFullKeys = 64;
+// Full-key tiles when on average over the probed coordinates at least this
+// many files share the high 16-bit key half of the median.  The half-key
+// tiles read back the low half of every such file, so their extra time
+// follows the mean count: 28 files tied with the median (ALIE colluders
+// sending the honest mean, K = 15) cost the half-key single pass about as
+// much as the full-key tiles cost, and data tied on a fraction x of the
+// coordinates (455 files each there) costs about x times the fully tied
+// case.  The mean, unlike a typical coordinate's count, sees ties that
+// cover less than half of the coordinates.
+constexpr uint32_t kTieFullKeys = 16;
 
-// The tie estimate: the median over the probed coordinates of the number
-// of files tied with the median's high key half (launch_tie_probe).
+// The tie estimate: the mean, rounded up, over the probed coordinates of
+// the number of files tied with the median's high key half
+// (launch_tie_probe).
 uint32_t tie_estimate(const uint32_t *counts, int n) {
-    uint32_t v[aspis::kTieCols];
-    for (int j = 0; j < n; ++j) v[j] = counts[j];
-    for (int j = 1; j < n; ++j)
-        for (int i = j; i > 0 && v[i - 1] > v[i]; --i) {
-            const uint32_t t = v[i];
-            v[i] = v[i - 1];
-            v[i - 1] = t;
-        }
-    return n > 0 ? v[n / 2] : 0u;
+    uint64_t sum = 0;
+    for (int j = 0; j < n; ++j) sum += counts[j];
+    return n > 0 ? (uint32_t)((sum + (uint64_t)n - 1) / (uint64_t)n) : 0u;
 }
 
 aspis_status check_detect_out(const aspis_detect_out *o) {
